@@ -1,0 +1,142 @@
+"""Planted mistakes: each test loads a copy of one oracle module with one
+plausible error written into it (a dropped term, a wrong sign, a wrong index,
+a transposed operand) and checks that an independent pin rejects it.  The
+mistakes live only in these in-memory copies, on the CPU."""
+
+import os
+import types
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import ModelDims, param_count, unpack_params
+
+ORACLE_DIR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle")
+
+
+def _mutant(module_file, old, new):
+    src = open(os.path.join(ORACLE_DIR, module_file)).read()
+    assert src.count(old) == 1, (module_file, old)
+    mod = types.ModuleType("oracle._mutant")
+    mod.__package__ = "oracle"
+    exec(compile(src.replace(old, new), module_file, "exec"), mod.__dict__)
+    return mod
+
+
+D = ModelDims(layers=2, input_dim=3, hidden=4, classes=5)
+
+
+def _torch_logits_and_grad(params, x, T, B, W):
+    layers, out = unpack_params(params, D)
+    lstm = torch.nn.LSTM(D.input_dim, D.hidden, num_layers=D.layers, dtype=torch.float64)
+    with torch.no_grad():
+        for l, p in enumerate(layers):
+            getattr(lstm, f"weight_ih_l{l}").copy_(torch.from_numpy(p["Wx"]))
+            getattr(lstm, f"weight_hh_l{l}").copy_(torch.from_numpy(p["Wh"]))
+            getattr(lstm, f"bias_ih_l{l}").copy_(torch.from_numpy(p["b"]))
+            getattr(lstm, f"bias_hh_l{l}").zero_()
+    Wo = torch.tensor(out["Wo"], requires_grad=True)
+    bo = torch.tensor(out["bo"], requires_grad=True)
+    h, _ = lstm(torch.from_numpy(x.reshape(T, B, D.input_dim)))
+    z = h.reshape(T * B, D.hidden) @ Wo.T + bo
+    (torch.from_numpy(W) * z).sum().backward()
+    g = np.zeros_like(params)
+    gl, go = unpack_params(g, D)
+    for l in range(D.layers):
+        gl[l]["Wx"][...] = getattr(lstm, f"weight_ih_l{l}").grad.numpy()
+        gl[l]["Wh"][...] = getattr(lstm, f"weight_hh_l{l}").grad.numpy()
+        gl[l]["b"][...] = getattr(lstm, f"bias_ih_l{l}").grad.numpy()
+    go["Wo"][...] = Wo.grad.numpy()
+    go["bo"][...] = bo.grad.numpy()
+    return z.detach().numpy(), g
+
+
+def _lstm_pins_pass(mod):
+    """True when the module's forward/backward agree with torch.nn.LSTM."""
+    T, B = 5, 3
+    rng = np.random.default_rng(0)
+    params = rng.uniform(-0.6, 0.6, size=param_count(D))
+    x = rng.standard_normal((T * B, D.input_dim))
+    W = rng.standard_normal((T * B, D.classes))
+    logits, cache = mod.lstm_am_forward(params, D, x, T, B)
+    grad = mod.lstm_am_backward(params, D, cache, W)
+    tz, tg = _torch_logits_and_grad(params, x, T, B, W)
+    return np.allclose(logits, tz, rtol=0, atol=1e-12) and np.allclose(grad, tg, rtol=1e-10, atol=1e-12)
+
+
+def test_unmutated_oracle_passes_lstm_pins():
+    assert _lstm_pins_pass(oracle.lstm_am)
+
+
+@pytest.mark.parametrize("old,new", [
+    ("c_new = gf * c[:nb] + gi * gg", "c_new = gi * c[:nb] + gf * gg"),     # gates swapped
+    ("go = _sigm(a[:, 3 * H:4 * H])", "go = _sigm(a[:, 2 * H:3 * H])"),     # wrong gate slice
+    ("h[:nb] @ p[\"Wh\"].T", "h[:nb] @ p[\"Wh\"][:, ::-1].T"),              # wrong index
+    ("dc = dh * go * (1.0 - tc * tc) + dc_next[:nb]", "dc = dh * go * (1.0 - tc * tc)"),  # dropped term
+    ("d_f = dc * c_prev", "d_f = dc * c"),                                    # wrong time index
+    ("d_g * (1.0 - gg * gg)", "d_g * (1.0 + gg * gg)"),                       # wrong sign
+    ("glayers[l][\"Wh\"][...] = dA.T @ cl[\"Hs\"]", "glayers[l][\"Wh\"][...] = dA.T @ cl[\"H\"]"),
+    ("dh_next[:nb] = da @ p[\"Wh\"]", "dh_next[:nb] = da @ p[\"Wh\"] * 0.0"),
+    ("dH = dZ @ out[\"Wo\"]", "dH = dZ @ out[\"Wo\"] * 2.0"),
+])
+def test_lstm_mistakes_are_caught(old, new):
+    assert not _lstm_pins_pass(_mutant("lstm_am.py", old, new))
+
+
+def _ce_pins_pass(mod):
+    rng = np.random.default_rng(1)
+    N, C = 12, 9
+    z = rng.standard_normal((N, C)) * 2
+    P = rng.dirichlet(np.full(C, 0.5), size=N) * 0.9
+    idx = np.stack([rng.permutation(C) for _ in range(N)])
+    prob = np.take_along_axis(P, idx, axis=1)
+    loss, dz = mod.sparse_soft_ce(z, idx, prob)
+    zt = torch.tensor(z, requires_grad=True)
+    tl = torch.nn.functional.cross_entropy(zt, torch.tensor(P))
+    tl.backward()
+    return abs(loss - tl.item()) <= 1e-12 * abs(tl.item()) and np.allclose(dz, zt.grad.numpy(), rtol=1e-10, atol=1e-15)
+
+
+def test_unmutated_oracle_passes_ce_pins():
+    assert _ce_pins_pass(oracle.soft_ce)
+
+
+@pytest.mark.parametrize("old,new", [
+    ("dz[f] = scale[f] * (mass * q - target)", "dz[f] = scale[f] * (q - target)"),   # mass dropped
+    ("lf -= p[f, j] * (z[f, c] - lse)", "lf -= p[f, j] * (z[f, c] + lse)"),          # sign
+    ("lse = zmax + np.log", "lse = np.log"),                                          # max not restored
+])
+def test_ce_mistakes_are_caught(old, new):
+    assert not _ce_pins_pass(_mutant("soft_ce.py", old, new))
+
+
+def _gtc_pins_pass(mod):
+    tau = np.float32(2.0 ** -10)
+    rng = np.random.default_rng(2)
+    n = 20000
+    g = (rng.integers(-5000, 5000, n) * 2.0 ** -20).astype(np.float32)
+    r = (rng.integers(-1500, 1500, n) * 2.0 ** -20).astype(np.float32)
+    g[:4] = [tau, -tau, 0, 0]
+    r[:4] = 0
+    new_r, words, count = mod.grad_threshold_encode(g, r, tau)
+    sent = mod.grad_threshold_decode(words, count, tau, n)
+    conserved = np.array_equal(new_r.astype(np.float64) + sent, r.astype(np.float64) + g)
+    strict = not np.any(np.isin(words >> 1, [0, 1]))
+    ascending = bool(np.all(np.diff(words >> 1) > 0))
+    return conserved and strict and ascending
+
+
+def test_unmutated_oracle_passes_gtc_pins():
+    assert _gtc_pins_pass(oracle.gtc)
+
+
+@pytest.mark.parametrize("old,new", [
+    ("pos = a > tau", "pos = a >= tau"),                                  # non-strict test
+    ("new_r[pos] = a[pos] - tau", "new_r[pos] = a[pos] + tau"),           # wrong sign
+    ("    a = r + g\n", "    a = g\n"),                                       # residual dropped
+    ("value = np.where((w & np.uint32(1)) != 0, -tau, tau)", "value = np.where((w & np.uint32(1)) != 0, tau, -tau)"),
+])
+def test_gtc_mistakes_are_caught(old, new):
+    assert not _gtc_pins_pass(_mutant("gtc.py", old, new))
