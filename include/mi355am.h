@@ -1,0 +1,197 @@
+/*
+ * mi355am.h -- C ABI of the MI355X (gfx950) student training step.
+ *
+ * The operation set is the per-worker hot path of data-parallel acoustic
+ * model training in Parthasarathi et al., "Realizing Petabyte Scale Acoustic
+ * Modeling": the student LSTM acoustic model (§II-B, §V-A) trained with
+ * chunked BPTT (§II-B, §V-D) against sparse k-best teacher posteriors
+ * (§II-C, §V-C) by mini-batch SGD (§VI, §VI-B), whose gradient is passed
+ * through Gradient Threshold Compression with residual error feedback (§VI-A).
+ *
+ * Conventions for every entry point:
+ *  - Pointers are device pointers unless the comment says [host].
+ *  - `stream` is a hipStream_t (NULL = the default stream).  All work is
+ *    enqueued on it asynchronously; nothing is synchronised unless stated.
+ *  - The caller owns every buffer.  No entry point allocates device memory;
+ *    scratch space is a caller-provided workspace `ws` of at least the size
+ *    returned by the matching *_workspace_bytes query (256-byte aligned).
+ *  - Arguments are validated on the host before anything is enqueued; on any
+ *    error nothing is enqueued and no buffer is touched.  The return value is
+ *    an am_status; am_last_error() gives a message for the calling thread.
+ *  - Values inside device buffers (target indices, counts) are not checked.
+ *
+ * Model and tensor layouts:
+ *  - am_model { layers L, input_dim D0, hidden H, classes C, dtype }.
+ *    dtype AM_F32: parameters, inputs and activations are fp32.
+ *    dtype AM_BF16: parameters (a bf16 working copy of fp32 master weights),
+ *    input frames, stored activations and dlogits are bf16; every product is
+ *    accumulated in fp32; cell states, logits and gradients are fp32.
+ *    Requirements: H % 16 == 0; D0, H and C multiples of 8 (bf16) or 4 (f32).
+ *  - Flat parameter vector (one buffer, so the whole gradient is quantised in
+ *    one call): for each layer l, Wx_l [4H][D_l], Wh_l [4H][H], b_l [4H]
+ *    (D_0 = D0, D_l = H), then Wo [C][H], bo [C].  Gate blocks along every
+ *    4H axis are ordered input, forget, cell candidate, output.
+ *  - Frames are packed time-major.  A batch is B sequences sorted by
+ *    non-increasing length (`lengths`, [host] int32[B], each in [0, T]), or B
+ *    sequences of T frames when `lengths` is NULL.  B_t = number of
+ *    sequences longer than t; frame (t, b), b < B_t, is row off_t + b with
+ *    off_t = B_0 + ... + B_{t-1}.  N = off_T rows in total; padding does not
+ *    exist.  Variable-length batches allow B <= 1024.
+ */
+#ifndef MI355AM_H
+#define MI355AM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  AM_OK = 0,
+  AM_EINVAL = -1,        /* bad pointer, size, layout or ordering */
+  AM_ECAPACITY = -2,     /* an output buffer is too small */
+  AM_EUNSUPPORTED = -3,  /* valid but outside what the kernels handle */
+  AM_EHIP = -4,          /* a HIP call failed (launch error, ...) */
+  AM_EWORKSPACE = -5     /* workspace missing or too small */
+} am_status;
+
+typedef enum { AM_F32 = 0, AM_BF16 = 1 } am_dtype;
+typedef enum { AM_MEAN_VALID = 0, AM_SUM = 1 } am_reduction;
+
+typedef struct {
+  int32_t layers;
+  int32_t input_dim;
+  int32_t hidden;
+  int32_t classes;
+  int32_t dtype; /* am_dtype */
+} am_model;
+
+/* ---- host-only queries ------------------------------------------------- */
+
+/* Number of parameters n of the model (24,145,848 for L=5, D0=192, H=768,
+ * C=3000), or -1 if the model description is invalid. */
+int64_t am_param_count(const am_model* m);
+
+/* Writes the 3L+2 start offsets (elements) of Wx_0, Wh_0, b_0, ..., Wo, bo
+ * into `offsets` [host]. */
+am_status am_param_offsets(const am_model* m, int64_t* offsets);
+
+/* Bytes of workspace lstm_am_forward/lstm_am_backward need for a batch of B
+ * sequences, T steps and N packed frames; -1 if invalid. */
+int64_t am_workspace_bytes(const am_model* m, int32_t T, int32_t B, int64_t N);
+
+/* Workspace for sparse_soft_ce over N rows / for grad_threshold_encode. */
+int64_t am_ce_workspace_bytes(int64_t N);
+int64_t am_encode_workspace_bytes(int64_t n);
+
+const char* am_status_string(int32_t status);
+const char* am_last_error(void);
+
+/* ---- the training step ------------------------------------------------- */
+
+/* Forward pass of the student LSTM acoustic model (§II-B): per layer and
+ * step, a = Wx x_t + Wh h_{t-1} + b; i, f, o = sigmoid, g = tanh of the gate
+ * blocks; c_t = f c_{t-1} + i g; h_t = o tanh(c_t); then logits
+ * z = Wo h^{L-1} + bo.
+ *   params  [n] model dtype;  x [N][D0] model dtype (packed frames)
+ *   lengths [host] [B] or NULL;  h0, c0 [L][B][H] fp32 or NULL (zero)
+ *   logits  [N][C] fp32 (written)
+ *   hT, cT  [L][B][H] fp32 or NULL: state after each sequence's last frame
+ *   ws      workspace; it keeps the activations lstm_am_backward consumes and
+ *           must not be modified between the two calls.                    */
+am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
+                          const int32_t* lengths, const float* h0, const float* c0,
+                          int32_t T, int32_t B, float* logits, float* hT, float* cT,
+                          void* ws, int64_t ws_bytes, void* stream);
+
+/* Cross-entropy between sparse teacher posteriors and the student softmax
+ * (§II-C, §V-A; k-best targets §V-C).  Per row f with mask m_f:
+ *   loss_f = -sum_j p_fj (z_{f,idx_fj} - logsumexp(z_f)),  M_f = sum_j p_fj,
+ *   dlogits_f = s_f (M_f softmax(z_f) - sum_j p_fj e_{idx_fj}),
+ *   loss = sum_f s_f loss_f,  s_f = m_f / sum(m) (AM_MEAN_VALID) or m_f (AM_SUM).
+ * Targets are used as given (no renormalisation); idx -1 marks an empty slot
+ * (any index outside [0, C) is treated as empty); repeated indices add.  Rows
+ * with m_f = 0 get zero gradient and their logits are not read.
+ * Requirements: C % 4 == 0, C <= 8192, logits 16-byte aligned.
+ *   logits [N][C] fp32;  idx [N][K] int32;  prob [N][K] fp32
+ *   mask   [N] uint8 or NULL (all valid);  loss [1] fp32 (written)
+ *   dlogits [N][C] of dlogits_dtype (AM_F32 or AM_BF16), written           */
+am_status sparse_soft_ce(int64_t N, int32_t C, int32_t K, const float* logits,
+                         const int32_t* idx, const float* prob, const uint8_t* mask,
+                         int32_t reduction, float* loss, void* dlogits,
+                         int32_t dlogits_dtype, void* ws, int64_t ws_bytes, void* stream);
+
+/* Back-propagation through time of the forward call that filled `ws`, given
+ * dL/dlogits (model dtype, [N][C]).  Writes the full gradient, fp32, in the
+ * flat parameter layout, into `grads` [n] (overwritten).  The state gradient
+ * is zero after each sequence's last frame (truncated BPTT within a chunk).
+ * Arguments m, params, x, lengths, T, B must be those of the forward call. */
+am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
+                           const int32_t* lengths, int32_t T, int32_t B,
+                           const void* dlogits, void* ws, int64_t ws_bytes,
+                           float* grads, void* stream);
+
+/* Gradient Threshold Compression encode (§VI-A), exact fp32:
+ *   for i in 0..n-1:  a = residual[i] + grad[i]
+ *     a >  tau: residual[i] = a - tau, emit (i << 1) | 0
+ *     a < -tau: residual[i] = a + tau, emit (i << 1) | 1
+ *     else:     residual[i] = a
+ * Words are written to `words` in ascending i; *count (device int64) gets
+ * their number.  NaN is never emitted.  n < 2^31; capacity >= n; tau > 0.
+ * `residual` is updated in place and is persistent trainer state.         */
+am_status grad_threshold_encode(int64_t n, const float* grad, float* residual, float tau,
+                                uint32_t* words, int64_t capacity, int64_t* count,
+                                void* ws, int64_t ws_bytes, void* stream);
+
+/* Decode (§VI-A): dense[i] = +tau (sign bit 0) or -tau (sign bit 1) for each
+ * of the first min(*count, capacity) words (count is a device int64, so no
+ * host synchronisation is needed; capacity = number of words `words` holds);
+ * accumulate = 0: every other element is +0.0;  accumulate = 1: dense[i] +=
+ * +-tau (one fp32 add per word) and other elements are left unchanged.
+ * Words must be strictly ascending in index, as encode writes them.        */
+am_status grad_threshold_decode(const uint32_t* words, const int64_t* count, int64_t capacity,
+                                float tau, int64_t n, float* dense, int32_t accumulate,
+                                void* stream);
+
+/* Local SGD step (§VI, §VI-B): master[i] = fl32(master[i] - lr * update[i])
+ * evaluated in fp64; weights_bf16[i] (uint16 bit patterns, or NULL) =
+ * round-to-nearest-even bf16 of the new master (NaN -> 0x7FC0).           */
+am_status sgd_apply(int64_t n, float* master, void* weights_bf16, const float* update,
+                    float lr, void* stream);
+
+/* fp32 -> bf16 (round to nearest even, NaN -> 0x7FC0), e.g. input frames. */
+am_status am_cast_f32_to_bf16(int64_t n, const float* src, void* dst_bf16, void* stream);
+
+/* ---- kernel timing ------------------------------------------------------ */
+
+/* Kernel classes for timing with HIP events. */
+typedef enum {
+  AM_K_GEMM_FWD = 0,      /* input and output projections */
+  AM_K_GEMM_BWD_DATA = 1, /* gradients into activations (dlogits Wo, dA Wx) */
+  AM_K_GEMM_BWD_WGT = 2,  /* weight gradients (reductions over frames) */
+  AM_K_LSTM_FWD = 3,      /* recurrent product + cell, one step */
+  AM_K_LSTM_BWD = 4,      /* recurrent product + cell backward, one step */
+  AM_K_CE = 5,            /* soft-target cross-entropy rows */
+  AM_K_ENCODE = 6,        /* threshold encode (all of its kernels) */
+  AM_K_DECODE = 7,
+  AM_K_SGD = 8,
+  AM_K_MISC = 9,          /* casts, transposes, bias reductions, gathers */
+  AM_K_NCLASSES = 10
+} am_kernel_class;
+
+/* Starts recording: every later launch of a class whose bit is set in
+ * `class_mask` is bracketed by HIP events on its stream.  Clears earlier
+ * records.  Not thread-safe; one recording at a time per process. */
+am_status am_profile_begin(uint32_t class_mask);
+/* Stops recording and synchronises on the recorded events. */
+am_status am_profile_end(void);
+/* Totals for one class since am_profile_begin: launches, summed kernel
+ * milliseconds, summed algorithmic flops and algorithmic HBM bytes. */
+am_status am_profile_get(int32_t kernel_class, int64_t* launches, double* ms,
+                         double* flops, double* bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MI355AM_H */

@@ -1,0 +1,100 @@
+// Device-side helpers shared by the gfx950 kernels of the training step.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace am {
+
+typedef uint16_t bf16_t;  // bf16 storage: upper half of an IEEE binary32
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// fp32 -> bf16, round to nearest even; NaN becomes the quiet NaN 0x7FC0.
+__device__ __forceinline__ bf16_t f32_to_bf16(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)0x7FC0;
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) {
+  return __uint_as_float((uint32_t)b << 16);
+}
+
+// Activation storage type <-> fp32.
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<bf16_t>(bf16_t v) { return bf16_to_f32(v); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
+
+// One MFMA operand fragment: 8 consecutive k-elements of one row (A) or one
+// column (B) of a 16x16 output tile.  Lane l serves row/column l % 16 and
+// the k-octet l / 16 of a 32-wide k-step.  The same k-octet mapping is used
+// for both operands, so the product is independent of how the hardware
+// orders k inside an instruction.
+template <typename T> struct Frag;
+template <> struct Frag<bf16_t> { uint4 v; };
+template <> struct Frag<float> { float4 lo, hi; };
+
+template <typename T> __device__ __forceinline__ Frag<T> frag_zero();
+template <> __device__ __forceinline__ Frag<bf16_t> frag_zero<bf16_t>() {
+  Frag<bf16_t> f; f.v = make_uint4(0, 0, 0, 0); return f;
+}
+template <> __device__ __forceinline__ Frag<float> frag_zero<float>() {
+  Frag<float> f; f.lo = make_float4(0.f, 0.f, 0.f, 0.f); f.hi = f.lo; return f;
+}
+
+// 8 elements starting at p (16-byte aligned for bf16, 32-byte for fp32).
+template <typename T> __device__ __forceinline__ Frag<T> frag_load(const T* p);
+template <> __device__ __forceinline__ Frag<bf16_t> frag_load<bf16_t>(const bf16_t* p) {
+  Frag<bf16_t> f; f.v = *reinterpret_cast<const uint4*>(p); return f;
+}
+template <> __device__ __forceinline__ Frag<float> frag_load<float>(const float* p) {
+  Frag<float> f;
+  f.lo = reinterpret_cast<const float4*>(p)[0];
+  f.hi = reinterpret_cast<const float4*>(p)[1];
+  return f;
+}
+
+// acc(16x16) += A(16x32) * B(32x16).
+__device__ __forceinline__ void mma_16x16x32(f32x4_t& acc, const Frag<bf16_t>& a,
+                                             const Frag<bf16_t>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a.v),
+                                                __builtin_bit_cast(bf16x8_t, b.v), acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma_16x16x32(f32x4_t& acc, const Frag<float>& a,
+                                             const Frag<float>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.x, b.lo.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.y, b.lo.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.z, b.lo.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.w, b.lo.w, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.x, b.hi.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.y, b.hi.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.z, b.hi.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.w, b.hi.w, acc, 0, 0, 0);
+}
+
+// Output tile layout of a 16x16 MFMA: lane l holds rows 4*(l/16)+r, r=0..3,
+// of column l%16.
+__device__ __forceinline__ int mfma_row(int lane, int r) { return 4 * (lane >> 4) + r; }
+__device__ __forceinline__ int mfma_col(int lane) { return lane & 15; }
+
+__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
+__device__ __forceinline__ float tanh_f(float x) { return tanhf(x); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+}  // namespace am

@@ -1,0 +1,100 @@
+// Host-side launchers of the gfx950 kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace am {
+
+// C[M][N] = sum_k A(m,k) B(k,n) (+ bias[n]).
+//   A(m,k) = A[m*lda + k] if a_kmajor else A[k*lda + m]
+//   B(k,n) = B[n*ldb + k] if b_kmajor else B[k*ldb + n]
+// Inputs are bf16 (bf16 = true) or fp32; C is fp32 (c_f32) or the input type;
+// bias is per column, input type.  Requirements (checked by the caller):
+// 16-byte aligned rows; a k-major K and an m/n-major M or N that is a
+// multiple of 8 (bf16) / 4 (fp32).
+struct GemmArgs {
+  const void* A; int64_t lda; bool a_kmajor;
+  const void* B; int64_t ldb; bool b_kmajor;
+  void* C; int64_t ldc; bool c_f32;
+  const void* bias;
+  int M, N, K;
+  bool bf16;
+};
+hipError_t gemm(const GemmArgs& g, hipStream_t s);
+
+// One forward step of one LSTM layer over the nb active rows of step t:
+// gate pre-activations P (input projection + bias, rows of step t) plus
+// h_{t-1} Wh^T, the cell update, and the stores BPTT needs.
+struct LstmFwdStep {
+  const void* P;      // [nb][4H]
+  const void* Wh;     // [4H][H]
+  const void* hprev;  // [nb][H] rows of h_{t-1}, or null (zero state)
+  const float* cprev; // [nb][H] rows of c_{t-1}, or null
+  void* H;            // [nb][H] h_t (written)
+  void* Hs;           // [nb][H] copy of h_{t-1} for the Wh gradient (written)
+  float* C;           // [nb][H] c_t (written)
+  void* G;            // [nb][4H] gate activations i,f,g,o (written)
+  int nb, hidden;
+  bool bf16;
+};
+hipError_t lstm_fwd_step(const LstmFwdStep& a, hipStream_t s);
+
+// One reverse step: dh = dHa + dA_{t+1} Wh (rows < nbn), cell backward,
+// dA_t written; dc carries dc_{t+1} in and dc_t out per sequence.
+struct LstmBwdStep {
+  const void* dAnext; // [nbn][4H] rows of step t+1, or null
+  int nbn;
+  const void* WhT;    // [H][4H]
+  const void* dHa;    // [nb][H] gradient from the layer above / output
+  const void* G;      // [nb][4H]
+  const float* C;     // [nb][H]
+  const float* Cprev; // [nb][H] c_{t-1} rows, or null (zero)
+  float* dc;          // [B][H]
+  void* dA;           // [nb][4H] (written)
+  int nb, hidden;
+  bool bf16;
+};
+hipError_t lstm_bwd_step(const LstmBwdStep& a, hipStream_t s);
+
+// Sparse soft-target cross-entropy rows (see sparse_soft_ce in the C ABI).
+struct SoftCeArgs {
+  int64_t N; int C; int K;
+  const float* z; const int32_t* idx; const float* prob; const uint8_t* mask;
+  int reduction; float* loss; void* dz; bool dz_bf16;
+  float* ws_partials; int64_t n_partials; float* ws_scale;
+};
+int64_t soft_ce_partials(int64_t N);
+hipError_t soft_ce(const SoftCeArgs& a, hipStream_t s);
+
+// Threshold encode / decode.
+int64_t gtc_tiles(int64_t n);
+hipError_t gtc_encode(int64_t n, const float* g, float* r, float tau, uint32_t* words,
+                      int64_t* count, uint32_t* ws_mask, int32_t* ws_tile, hipStream_t s);
+hipError_t gtc_decode(const uint32_t* words, const int64_t* count, int64_t capacity, float tau,
+                      int64_t n, float* dense, bool accumulate, hipStream_t s);
+
+// Elementwise and data-movement helpers.
+hipError_t sgd_apply_f32(int64_t n, float* master, uint16_t* w_bf16, const float* u, float lr,
+                         hipStream_t s);
+hipError_t cast_f32_bf16(int64_t n, const float* src, uint16_t* dst, hipStream_t s);
+// dst[c][r] = src[r][c] for a rows x cols matrix of the activation type.
+hipError_t transpose(const void* src, void* dst, int rows, int cols, bool bf16, hipStream_t s);
+// out[c] = sum_r in[r][c] (fp32 result, fixed summation order).
+hipError_t colsum(const void* in, int64_t rows, int cols, bool bf16, float* out,
+                  float* ws_partial, int n_chunks, hipStream_t s);
+// dst[0..n) = +0.0 (a kernel, so the call is safe inside graph capture).
+hipError_t fill_zero(float* dst, int64_t n, hipStream_t s);
+// Convert fp32 [rows][cols] to the activation type (h0 for the recurrence).
+hipError_t convert_rows(const float* src, void* dst, int64_t count, bool bf16, hipStream_t s);
+// Final states: out[b][j] = state at row[b] (or init[b][j] / 0 if row[b] < 0).
+struct GatherState {
+  const void* Hrows; bool h_bf16; const float* Crows;
+  const float* h0; const float* c0;
+  float* hT; float* cT;
+  int B, hidden;
+  int rows[256];
+};
+hipError_t gather_state(const GatherState& a, int b0, int nb, hipStream_t s);
+
+}  // namespace am

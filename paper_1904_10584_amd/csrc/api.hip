@@ -1,0 +1,582 @@
+// C ABI of the training step (declared in include/mi355am.h): argument
+// validation, workspace planning, the launch sequence of the forward and
+// backward passes, and per-class kernel timing with HIP events.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/mi355am.h"
+#include "am_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+am_status fail(am_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+am_status hip_check(hipError_t e, const char* what) {
+  if (e == hipSuccess) return AM_OK;
+  return fail(AM_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define AM_TRY(expr)                        \
+  do {                                      \
+    am_status st_ = (expr);                 \
+    if (st_ != AM_OK) return st_;           \
+  } while (0)
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+// ---------------------------------------------------------------- timing --
+
+struct ProfRec {
+  int cls;
+  hipEvent_t a, b;
+  double flops, bytes;
+};
+
+struct Prof {
+  bool on = false;
+  uint32_t mask = 0;
+  std::vector<hipEvent_t> pool;
+  size_t next = 0;
+  std::vector<ProfRec> recs;
+  int64_t launches[AM_K_NCLASSES] = {};
+  double ms[AM_K_NCLASSES] = {}, flops[AM_K_NCLASSES] = {}, bytes[AM_K_NCLASSES] = {};
+} g_prof;
+
+hipEvent_t prof_event() {
+  if (g_prof.next == g_prof.pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    g_prof.pool.push_back(e);
+  }
+  return g_prof.pool[g_prof.next++];
+}
+
+// Brackets the kernels launched during its lifetime with events when the
+// class is being recorded.
+class Timed {
+ public:
+  Timed(int cls, hipStream_t s, double flops, double bytes) : s_(s) {
+    if (!g_prof.on || !(g_prof.mask & (1u << cls))) return;
+    rec_.cls = cls;
+    rec_.flops = flops;
+    rec_.bytes = bytes;
+    rec_.a = prof_event();
+    rec_.b = prof_event();
+    if (rec_.a && rec_.b && hipEventRecord(rec_.a, s_) == hipSuccess) active_ = true;
+  }
+  ~Timed() {
+    if (active_ && hipEventRecord(rec_.b, s_) == hipSuccess) g_prof.recs.push_back(rec_);
+  }
+
+ private:
+  hipStream_t s_;
+  ProfRec rec_{};
+  bool active_ = false;
+};
+
+// ------------------------------------------------------------- the model --
+
+int vec_of(int dtype) { return dtype == AM_BF16 ? 8 : 4; }
+int esz_of(int dtype) { return dtype == AM_BF16 ? 2 : 4; }
+
+am_status check_model(const am_model* m) {
+  if (!m) return fail(AM_EINVAL, "model is NULL");
+  if (m->dtype != AM_F32 && m->dtype != AM_BF16) return fail(AM_EINVAL, "dtype %d unknown", m->dtype);
+  if (m->layers < 1 || m->input_dim < 1 || m->hidden < 1 || m->classes < 1)
+    return fail(AM_EINVAL, "model sizes must be positive");
+  if (m->hidden % 16) return fail(AM_EUNSUPPORTED, "hidden %d is not a multiple of 16", m->hidden);
+  const int v = vec_of(m->dtype);
+  if (m->input_dim % v || m->classes % v)
+    return fail(AM_EUNSUPPORTED, "input_dim and classes must be multiples of %d for this dtype", v);
+  if ((int64_t)m->hidden * 4 * (int64_t)(m->hidden > m->input_dim ? m->hidden : m->input_dim) >= (1ll << 31))
+    return fail(AM_EUNSUPPORTED, "layer too large");
+  return AM_OK;
+}
+
+struct Offsets {
+  std::vector<int64_t> wx, wh, b;
+  int64_t wo, bo, n;
+};
+
+Offsets param_layout(const am_model* m) {
+  Offsets o;
+  const int64_t G = 4ll * m->hidden;
+  int64_t pos = 0;
+  for (int l = 0; l < m->layers; ++l) {
+    const int64_t D = l == 0 ? m->input_dim : m->hidden;
+    o.wx.push_back(pos); pos += G * D;
+    o.wh.push_back(pos); pos += G * m->hidden;
+    o.b.push_back(pos); pos += G;
+  }
+  o.wo = pos; pos += (int64_t)m->classes * m->hidden;
+  o.bo = pos; pos += m->classes;
+  o.n = pos;
+  return o;
+}
+
+// Schedule of a batch: active counts per step and packed row offsets.
+struct Schedule {
+  int T = 0, B = 0;
+  std::vector<int64_t> counts, offs;
+  std::vector<int32_t> lens;
+  int64_t N = 0;
+};
+
+am_status make_schedule(int32_t T, int32_t B, const int32_t* lengths, Schedule& s) {
+  if (T < 0 || B < 1) return fail(AM_EINVAL, "need T >= 0 and B >= 1 (T=%d, B=%d)", T, B);
+  s.T = T; s.B = B;
+  s.lens.assign(B, T);
+  if (lengths) {
+    if (B > 1024) return fail(AM_EUNSUPPORTED, "variable-length batches allow B <= 1024");
+    for (int b = 0; b < B; ++b) {
+      if (lengths[b] < 0 || lengths[b] > T)
+        return fail(AM_EINVAL, "lengths[%d] = %d outside [0, %d]", b, lengths[b], T);
+      if (b > 0 && lengths[b] > lengths[b - 1])
+        return fail(AM_EINVAL, "lengths must be non-increasing (lengths[%d] > lengths[%d])", b, b - 1);
+      s.lens[b] = lengths[b];
+    }
+  }
+  s.counts.assign(T, 0);
+  s.offs.assign(T + 1, 0);
+  int64_t nb = B;
+  for (int t = 0; t < T; ++t) {
+    while (nb > 0 && s.lens[nb - 1] <= t) --nb;
+    s.counts[t] = nb;
+    s.offs[t + 1] = s.offs[t] + nb;
+  }
+  s.N = s.offs[T];
+  if (s.N >= (1ll << 31)) return fail(AM_EUNSUPPORTED, "too many frames");
+  return AM_OK;
+}
+
+// Workspace carve-up (256-byte aligned regions).
+struct WsLayout {
+  std::vector<int64_t> h, hs, c, g;  // per layer
+  int64_t p_da, dh, wht, dc, c0, h0, colsum, total;
+  static constexpr int COLSUM_CHUNKS = 64;
+};
+
+int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+WsLayout ws_layout(const am_model* m, int64_t B, int64_t N) {
+  WsLayout w;
+  const int64_t e = esz_of(m->dtype), H = m->hidden, G = 4 * H, L = m->layers;
+  int64_t pos = 0;
+  auto take = [&](int64_t bytes) { int64_t at = pos; pos += align256(bytes); return at; };
+  for (int l = 0; l < L; ++l) {
+    w.h.push_back(take(N * H * e));
+    w.hs.push_back(take(N * H * e));
+    w.c.push_back(take(N * H * 4));
+    w.g.push_back(take(N * G * e));
+  }
+  w.p_da = take(N * G * e);
+  w.dh = take(N * H * e);
+  w.wht = take(G * H * e);
+  w.dc = take(B * H * 4);
+  w.c0 = take(L * B * H * 4);
+  w.h0 = take(L * B * H * e);
+  const int64_t cols = G > m->classes ? G : m->classes;
+  w.colsum = take(WsLayout::COLSUM_CHUNKS * cols * 4);
+  w.total = pos;
+  return w;
+}
+
+template <typename P> P* at(void* base, int64_t off) {
+  return reinterpret_cast<P*>(static_cast<char*>(base) + off);
+}
+
+double gemm_bytes(int64_t M, int64_t N, int64_t K, int64_t e, int64_t out) {
+  return (double)(M * K + N * K) * e + (double)(M * N) * out;
+}
+
+am_status run_gemm(int cls, const am::GemmArgs& g, hipStream_t s) {
+  const int64_t e = g.bf16 ? 2 : 4;
+  Timed tm(cls, s, 2.0 * g.M * g.N * (double)g.K, gemm_bytes(g.M, g.N, g.K, e, g.c_f32 ? 4 : e));
+  return hip_check(am::gemm(g, s), "gemm");
+}
+
+am::GemmArgs mk_gemm(const void* A, int64_t lda, bool ak, const void* B, int64_t ldb, bool bk,
+                     void* C, int64_t ldc, bool cf32, const void* bias, int M, int N, int K,
+                     bool bf16) {
+  am::GemmArgs g;
+  g.A = A; g.lda = lda; g.a_kmajor = ak;
+  g.B = B; g.ldb = ldb; g.b_kmajor = bk;
+  g.C = C; g.ldc = ldc; g.c_f32 = cf32;
+  g.bias = bias; g.M = M; g.N = N; g.K = K; g.bf16 = bf16;
+  return g;
+}
+
+}  // namespace
+
+// ================================================================= C ABI ==
+
+extern "C" {
+
+const char* am_status_string(int32_t st) {
+  switch (st) {
+    case AM_OK: return "ok";
+    case AM_EINVAL: return "invalid argument";
+    case AM_ECAPACITY: return "output capacity too small";
+    case AM_EUNSUPPORTED: return "unsupported configuration";
+    case AM_EHIP: return "HIP error";
+    case AM_EWORKSPACE: return "workspace missing or too small";
+    default: return "unknown status";
+  }
+}
+
+const char* am_last_error(void) { return g_err.c_str(); }
+
+int64_t am_param_count(const am_model* m) {
+  if (check_model(m) != AM_OK) return -1;
+  return param_layout(m).n;
+}
+
+am_status am_param_offsets(const am_model* m, int64_t* offsets) {
+  AM_TRY(check_model(m));
+  if (!offsets) return fail(AM_EINVAL, "offsets is NULL");
+  Offsets o = param_layout(m);
+  for (int l = 0; l < m->layers; ++l) {
+    offsets[3 * l] = o.wx[l];
+    offsets[3 * l + 1] = o.wh[l];
+    offsets[3 * l + 2] = o.b[l];
+  }
+  offsets[3 * m->layers] = o.wo;
+  offsets[3 * m->layers + 1] = o.bo;
+  return AM_OK;
+}
+
+int64_t am_workspace_bytes(const am_model* m, int32_t T, int32_t B, int64_t N) {
+  if (check_model(m) != AM_OK || T < 0 || B < 1 || N < 0 || N > (int64_t)T * B) return -1;
+  return ws_layout(m, B, N).total;
+}
+
+int64_t am_ce_workspace_bytes(int64_t N) {
+  if (N < 0) return -1;
+  return align256(am::soft_ce_partials(N) * 4) + 256;
+}
+
+int64_t am_encode_workspace_bytes(int64_t n) {
+  if (n < 0) return -1;
+  const int64_t tiles = am::gtc_tiles(n);
+  return align256(tiles * 256 * 4) + align256(tiles * 4);
+}
+
+am_status am_cast_f32_to_bf16(int64_t n, const float* src, void* dst, void* stream) {
+  if (n < 0) return fail(AM_EINVAL, "n < 0");
+  if (n > 0 && (!src || !dst)) return fail(AM_EINVAL, "NULL pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Timed tm(AM_K_MISC, s, 0.0, 6.0 * n);
+  return hip_check(am::cast_f32_bf16(n, src, static_cast<uint16_t*>(dst), s), "cast");
+}
+
+am_status sgd_apply(int64_t n, float* master, void* weights_bf16, const float* update, float lr,
+                    void* stream) {
+  if (n < 0) return fail(AM_EINVAL, "n < 0");
+  if (n > 0 && (!master || !update)) return fail(AM_EINVAL, "NULL pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Timed tm(AM_K_SGD, s, 2.0 * n, (weights_bf16 ? 14.0 : 12.0) * n);
+  return hip_check(am::sgd_apply_f32(n, master, static_cast<uint16_t*>(weights_bf16), update, lr, s),
+                   "sgd_apply");
+}
+
+am_status grad_threshold_encode(int64_t n, const float* grad, float* residual, float tau,
+                                uint32_t* words, int64_t capacity, int64_t* count, void* ws,
+                                int64_t ws_bytes, void* stream) {
+  if (n < 0 || n >= (1ll << 31)) return fail(AM_EINVAL, "n = %lld outside [0, 2^31)", (long long)n);
+  if (!(tau > 0.f)) return fail(AM_EINVAL, "tau must be > 0");
+  if (!count) return fail(AM_EINVAL, "count is NULL");
+  if (n > 0 && (!grad || !residual || !words)) return fail(AM_EINVAL, "NULL pointer");
+  if (capacity < n) return fail(AM_ECAPACITY, "capacity %lld < n %lld", (long long)capacity, (long long)n);
+  const int64_t need = am_encode_workspace_bytes(n);
+  if (!ws || ws_bytes < need || !aligned(ws, 256))
+    return fail(AM_EWORKSPACE, "encode needs %lld workspace bytes (256-aligned)", (long long)need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t tiles = am::gtc_tiles(n);
+  uint32_t* codes = at<uint32_t>(ws, 0);
+  int32_t* tile = at<int32_t>(ws, align256(tiles * 256 * 4));
+  Timed tm(AM_K_ENCODE, s, 0.0, 12.0 * n);
+  return hip_check(am::gtc_encode(n, grad, residual, tau, words, count, codes, tile, s), "encode");
+}
+
+am_status grad_threshold_decode(const uint32_t* words, const int64_t* count, int64_t capacity,
+                                float tau, int64_t n, float* dense, int32_t accumulate,
+                                void* stream) {
+  if (n < 0 || n >= (1ll << 31)) return fail(AM_EINVAL, "n outside [0, 2^31)");
+  if (capacity < 0) return fail(AM_EINVAL, "capacity < 0");
+  if (!count || (n > 0 && !dense) || (capacity > 0 && !words)) return fail(AM_EINVAL, "NULL pointer");
+  if (accumulate != 0 && accumulate != 1) return fail(AM_EINVAL, "accumulate must be 0 or 1");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Timed tm(AM_K_DECODE, s, 0.0, (accumulate ? 8.0 : 4.0) * n);
+  return hip_check(am::gtc_decode(words, count, capacity, tau, n, dense, accumulate != 0, s), "decode");
+}
+
+am_status sparse_soft_ce(int64_t N, int32_t C, int32_t K, const float* logits, const int32_t* idx,
+                         const float* prob, const uint8_t* mask, int32_t reduction, float* loss,
+                         void* dlogits, int32_t dlogits_dtype, void* ws, int64_t ws_bytes,
+                         void* stream) {
+  if (N < 0 || C < 1 || K < 0) return fail(AM_EINVAL, "need N >= 0, C >= 1, K >= 0");
+  if (C % 4) return fail(AM_EUNSUPPORTED, "C must be a multiple of 4");
+  if (C > 8192) return fail(AM_EUNSUPPORTED, "C > 8192 classes");
+  if (reduction != AM_MEAN_VALID && reduction != AM_SUM) return fail(AM_EINVAL, "unknown reduction");
+  if (dlogits_dtype != AM_F32 && dlogits_dtype != AM_BF16) return fail(AM_EINVAL, "unknown dlogits dtype");
+  if (!loss) return fail(AM_EINVAL, "loss is NULL");
+  if (N > 0 && (!logits || !dlogits || (K > 0 && (!idx || !prob))))
+    return fail(AM_EINVAL, "NULL pointer");
+  if (!aligned(logits, 16) || !aligned(dlogits, dlogits_dtype == AM_BF16 ? 8 : 16))
+    return fail(AM_EINVAL, "logits / dlogits must be 16-byte aligned");
+  const int64_t need = am_ce_workspace_bytes(N);
+  if (!ws || ws_bytes < need || !aligned(ws, 256))
+    return fail(AM_EWORKSPACE, "soft_ce needs %lld workspace bytes (256-aligned)", (long long)need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  am::SoftCeArgs a;
+  a.N = N; a.C = C; a.K = K; a.z = logits; a.idx = idx; a.prob = prob; a.mask = mask;
+  a.reduction = reduction; a.loss = loss; a.dz = dlogits; a.dz_bf16 = dlogits_dtype == AM_BF16;
+  a.n_partials = am::soft_ce_partials(N);
+  a.ws_partials = at<float>(ws, 0);
+  a.ws_scale = at<float>(ws, align256(a.n_partials * 4));
+  const double bytes = (double)N * C * (4 + (a.dz_bf16 ? 2 : 4)) + (double)N * K * 8;
+  Timed tm(AM_K_CE, s, 0.0, bytes);
+  return hip_check(am::soft_ce(a, s), "sparse_soft_ce");
+}
+
+am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
+                          const int32_t* lengths, const float* h0, const float* c0, int32_t T,
+                          int32_t B, float* logits, float* hT, float* cT, void* ws,
+                          int64_t ws_bytes, void* stream) {
+  AM_TRY(check_model(m));
+  Schedule sc;
+  AM_TRY(make_schedule(T, B, lengths, sc));
+  if (!params || !ws) return fail(AM_EINVAL, "NULL params or workspace");
+  if (sc.N > 0 && (!x || !logits)) return fail(AM_EINVAL, "NULL x or logits");
+  if (!aligned(params, 16) || !aligned(x, 16) || !aligned(logits, 16) || !aligned(ws, 256))
+    return fail(AM_EINVAL, "params, x, logits must be 16-byte and ws 256-byte aligned");
+  const WsLayout w = ws_layout(m, B, sc.N);
+  if (ws_bytes < w.total)
+    return fail(AM_EWORKSPACE, "forward needs %lld workspace bytes", (long long)w.total);
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf = m->dtype == AM_BF16;
+  const int64_t e = esz_of(m->dtype), H = m->hidden, G = 4 * H, L = m->layers;
+  const Offsets po = param_layout(m);
+  const char* P8 = static_cast<const char*>(params);
+
+  // initial cell state (copied, or zero) and initial hidden state (converted)
+  {
+    Timed tm(AM_K_MISC, s, 0.0, 8.0 * L * B * H);
+    float* c0w = at<float>(ws, w.c0);
+    if (c0) AM_TRY(hip_check(am::convert_rows(c0, c0w, L * B * H, false, s), "c0 copy"));
+    else AM_TRY(hip_check(am::fill_zero(c0w, L * B * H, s), "c0 clear"));
+    if (h0) AM_TRY(hip_check(am::convert_rows(h0, at<void>(ws, w.h0), L * B * H, bf, s), "h0 convert"));
+  }
+
+  for (int l = 0; l < L; ++l) {
+    const int64_t D = l == 0 ? m->input_dim : H;
+    const void* X = l == 0 ? x : at<void>(ws, w.h[l - 1]);
+    void* P = at<void>(ws, w.p_da);
+    AM_TRY(run_gemm(AM_K_GEMM_FWD,
+                    mk_gemm(X, D, true, P8 + po.wx[l] * e, D, true, P, G, false, P8 + po.b[l] * e,
+                            (int)sc.N, (int)G, (int)D, bf), s));
+    const char* Hl = at<char>(ws, w.h[l]);
+    const float* Cl = at<float>(ws, w.c[l]);
+    for (int t = 0; t < T; ++t) {
+      const int64_t nb = sc.counts[t];
+      if (nb == 0) break;
+      const int64_t o = sc.offs[t];
+      am::LstmFwdStep a;
+      a.P = at<char>(ws, w.p_da) + o * G * e;
+      a.Wh = P8 + po.wh[l] * e;
+      if (t == 0) {
+        a.hprev = h0 ? at<char>(ws, w.h0) + (int64_t)l * B * H * e : nullptr;
+        a.cprev = at<float>(ws, w.c0) + (int64_t)l * B * H;
+      } else {
+        a.hprev = Hl + sc.offs[t - 1] * H * e;
+        a.cprev = Cl + sc.offs[t - 1] * H;
+      }
+      a.H = at<char>(ws, w.h[l]) + o * H * e;
+      a.Hs = at<char>(ws, w.hs[l]) + o * H * e;
+      a.C = at<float>(ws, w.c[l]) + o * H;
+      a.G = at<char>(ws, w.g[l]) + o * G * e;
+      a.nb = (int)nb;
+      a.hidden = (int)H;
+      a.bf16 = bf;
+      const double bytes = (double)(nb * H + G * H + nb * G) * e + nb * H * 4.0 +
+                           (double)nb * (H * (2 * e + 4) + G * e);
+      Timed tm(AM_K_LSTM_FWD, s, 2.0 * nb * G * H, bytes);
+      AM_TRY(hip_check(am::lstm_fwd_step(a, s), "lstm forward step"));
+    }
+  }
+  AM_TRY(run_gemm(AM_K_GEMM_FWD,
+                  mk_gemm(at<void>(ws, w.h[L - 1]), H, true, P8 + po.wo * e, H, true, logits,
+                          m->classes, true, P8 + po.bo * e, (int)sc.N, m->classes, (int)H, bf), s));
+
+  if (hT || cT) {
+    for (int l = 0; l < L; ++l) {
+      for (int b0 = 0; b0 < B; b0 += 256) {
+        am::GatherState g;
+        g.Hrows = at<void>(ws, w.h[l]);
+        g.h_bf16 = bf;
+        g.Crows = at<float>(ws, w.c[l]);
+        g.h0 = h0 ? h0 + (int64_t)l * B * H : nullptr;
+        g.c0 = c0 ? c0 + (int64_t)l * B * H : nullptr;
+        g.hT = hT ? hT + (int64_t)l * B * H : nullptr;
+        g.cT = cT ? cT + (int64_t)l * B * H : nullptr;
+        g.B = B;
+        g.hidden = (int)H;
+        const int nb = B - b0 < 256 ? B - b0 : 256;
+        for (int i = 0; i < nb; ++i) {
+          const int len = sc.lens[b0 + i];
+          g.rows[i] = len > 0 ? (int)(sc.offs[len - 1] + b0 + i) : -1;
+        }
+        Timed tm(AM_K_MISC, s, 0.0, 16.0 * nb * H);
+        AM_TRY(hip_check(am::gather_state(g, b0, nb, s), "final state"));
+      }
+    }
+  }
+  return AM_OK;
+}
+
+am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
+                           const int32_t* lengths, int32_t T, int32_t B, const void* dlogits,
+                           void* ws, int64_t ws_bytes, float* grads, void* stream) {
+  AM_TRY(check_model(m));
+  Schedule sc;
+  AM_TRY(make_schedule(T, B, lengths, sc));
+  if (!params || !ws || !grads) return fail(AM_EINVAL, "NULL params, workspace or grads");
+  if (sc.N > 0 && (!x || !dlogits)) return fail(AM_EINVAL, "NULL x or dlogits");
+  if (!aligned(params, 16) || !aligned(x, 16) || !aligned(dlogits, 16) || !aligned(grads, 16) ||
+      !aligned(ws, 256))
+    return fail(AM_EINVAL, "params, x, dlogits, grads must be 16-byte and ws 256-byte aligned");
+  const WsLayout w = ws_layout(m, B, sc.N);
+  if (ws_bytes < w.total)
+    return fail(AM_EWORKSPACE, "backward needs %lld workspace bytes", (long long)w.total);
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf = m->dtype == AM_BF16;
+  const int64_t e = esz_of(m->dtype), H = m->hidden, G = 4 * H, L = m->layers, Cc = m->classes;
+  const int N = (int)sc.N;
+  const Offsets po = param_layout(m);
+  const char* P8 = static_cast<const char*>(params);
+  float* colws = at<float>(ws, w.colsum);
+
+  // output layer: dWo = dZ^T H_top, dbo = column sums of dZ, dH_top = dZ Wo
+  AM_TRY(run_gemm(AM_K_GEMM_BWD_WGT,
+                  mk_gemm(dlogits, Cc, false, at<void>(ws, w.h[L - 1]), H, false, grads + po.wo, H,
+                          true, nullptr, (int)Cc, (int)H, N, bf), s));
+  {
+    Timed tm(AM_K_MISC, s, (double)N * Cc, (double)N * Cc * e);
+    AM_TRY(hip_check(am::colsum(dlogits, N, (int)Cc, bf, grads + po.bo, colws,
+                                WsLayout::COLSUM_CHUNKS, s), "bias gradient"));
+  }
+  void* DH = at<void>(ws, w.dh);
+  AM_TRY(run_gemm(AM_K_GEMM_BWD_DATA,
+                  mk_gemm(dlogits, Cc, true, P8 + po.wo * e, H, false, DH, H, false, nullptr, N,
+                          (int)H, (int)Cc, bf), s));
+
+  char* dA = at<char>(ws, w.p_da);
+  void* WhT = at<void>(ws, w.wht);
+  float* dc = at<float>(ws, w.dc);
+  for (int l = L - 1; l >= 0; --l) {
+    const int64_t D = l == 0 ? m->input_dim : H;
+    {
+      Timed tm(AM_K_MISC, s, 0.0, 2.0 * G * H * e);
+      AM_TRY(hip_check(am::transpose(P8 + po.wh[l] * e, WhT, (int)G, (int)H, bf, s), "Wh transpose"));
+    }
+    const char* Gl = at<char>(ws, w.g[l]);
+    const float* Cl = at<float>(ws, w.c[l]);
+    for (int t = T - 1; t >= 0; --t) {
+      const int64_t nb = sc.counts[t];
+      if (nb == 0) continue;
+      const int64_t nbn = t + 1 < T ? sc.counts[t + 1] : 0;
+      const int64_t o = sc.offs[t];
+      am::LstmBwdStep a;
+      a.dAnext = nbn > 0 ? dA + sc.offs[t + 1] * G * e : nullptr;
+      a.nbn = (int)nbn;
+      a.WhT = WhT;
+      a.dHa = static_cast<char*>(DH) + o * H * e;
+      a.G = Gl + o * G * e;
+      a.C = Cl + o * H;
+      a.Cprev = t == 0 ? at<float>(ws, w.c0) + (int64_t)l * B * H : Cl + sc.offs[t - 1] * H;
+      a.dc = dc;
+      a.dA = dA + o * G * e;
+      a.nb = (int)nb;
+      a.hidden = (int)H;
+      a.bf16 = bf;
+      const double bytes = (double)(nbn * G + G * H + nb * H + nb * G) * e +
+                           nb * H * 12.0 + (double)nb * G * e;
+      Timed tm(AM_K_LSTM_BWD, s, 2.0 * nbn * G * H, bytes);
+      AM_TRY(hip_check(am::lstm_bwd_step(a, s), "lstm backward step"));
+    }
+    const void* X = l == 0 ? x : at<void>(ws, w.h[l - 1]);
+    AM_TRY(run_gemm(AM_K_GEMM_BWD_WGT,
+                    mk_gemm(dA, G, false, X, D, false, grads + po.wx[l], D, true, nullptr, (int)G,
+                            (int)D, N, bf), s));
+    AM_TRY(run_gemm(AM_K_GEMM_BWD_WGT,
+                    mk_gemm(dA, G, false, at<void>(ws, w.hs[l]), H, false, grads + po.wh[l], H,
+                            true, nullptr, (int)G, (int)H, N, bf), s));
+    {
+      Timed tm(AM_K_MISC, s, (double)N * G, (double)N * G * e);
+      AM_TRY(hip_check(am::colsum(dA, N, (int)G, bf, grads + po.b[l], colws,
+                                  WsLayout::COLSUM_CHUNKS, s), "bias gradient"));
+    }
+    if (l > 0)
+      AM_TRY(run_gemm(AM_K_GEMM_BWD_DATA,
+                      mk_gemm(dA, G, true, P8 + po.wx[l] * e, D, false, DH, H, false, nullptr, N,
+                              (int)H, (int)G, bf), s));
+  }
+  return AM_OK;
+}
+
+// ---------------------------------------------------------------- timing --
+
+am_status am_profile_begin(uint32_t class_mask) {
+  g_prof.on = true;
+  g_prof.mask = class_mask;
+  g_prof.next = 0;
+  g_prof.recs.clear();
+  for (int k = 0; k < AM_K_NCLASSES; ++k) {
+    g_prof.launches[k] = 0;
+    g_prof.ms[k] = g_prof.flops[k] = g_prof.bytes[k] = 0.0;
+  }
+  return AM_OK;
+}
+
+am_status am_profile_end(void) {
+  g_prof.on = false;
+  for (const ProfRec& r : g_prof.recs) {
+    AM_TRY(hip_check(hipEventSynchronize(r.b), "event sync"));
+    float ms = 0.f;
+    AM_TRY(hip_check(hipEventElapsedTime(&ms, r.a, r.b), "event elapsed"));
+    g_prof.launches[r.cls] += 1;
+    g_prof.ms[r.cls] += ms;
+    g_prof.flops[r.cls] += r.flops;
+    g_prof.bytes[r.cls] += r.bytes;
+  }
+  g_prof.recs.clear();
+  return AM_OK;
+}
+
+am_status am_profile_get(int32_t cls, int64_t* launches, double* ms, double* flops, double* bytes) {
+  if (cls < 0 || cls >= AM_K_NCLASSES) return fail(AM_EINVAL, "unknown kernel class");
+  if (launches) *launches = g_prof.launches[cls];
+  if (ms) *ms = g_prof.ms[cls];
+  if (flops) *flops = g_prof.flops[cls];
+  if (bytes) *bytes = g_prof.bytes[cls];
+  return AM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,223 @@
+// Gradient Threshold Compression: encode with residual error feedback and
+// ordered compaction of the sent elements into (index << 1 | sign) words,
+// and the matching decode.  Exact fp32 (single adds/subtracts, IEEE
+// subnormals), so the result is bit-identical to the element-wise definition.
+//
+// Encode runs in three HBM-bound passes over tiles of 4096 elements:
+//   1. update: a = r + g; r <- a -+ tau where |a| > tau; a 2-bit code per
+//      element (sent, sign) is packed 16 codes per thread word; per-tile count.
+//      Reads g and r, writes r: 12 bytes per element plus 1/4 byte of codes.
+//   2. scan: exclusive prefix over the tile counts (one block) and the total.
+//   3. compact: each tile re-reads its 1 KB of codes, ranks the sent elements
+//      in index order and writes their words contiguously.
+// Decode builds each 4096-element tile of the dense update in LDS (zero or
+// the existing values, then +-tau at the indices of the tile's words, found
+// by binary search in the ascending word list) and writes it once.
+#include "am_device.h"
+#include "am_internal.h"
+
+namespace am {
+namespace {
+
+constexpr int TILE = 4096;        // elements per tile
+constexpr int TPB = 256;          // threads per block; 16 elements each
+// Element e of a tile is handled by thread (e % 1024) / 4 as item
+// (e / 1024) * 4 + e % 4: four float4 groups at stride 1024.
+
+template <bool ALIGNED>
+__global__ __launch_bounds__(TPB) void gtc_update(int64_t n, const float* __restrict__ g,
+                                                  float* __restrict__ r, float tau,
+                                                  uint32_t* __restrict__ codes,
+                                                  int32_t* __restrict__ tile_count) {
+  __shared__ int wsum[TPB / 64];
+  const int64_t base = (int64_t)blockIdx.x * TILE;
+  uint32_t code = 0;
+#pragma unroll
+  for (int grp = 0; grp < 4; ++grp) {
+    const int64_t e = base + grp * 1024 + threadIdx.x * 4;
+    float gv[4], rv[4];
+    if (ALIGNED && e + 3 < n) {
+      const float4 g4 = *reinterpret_cast<const float4*>(g + e);
+      const float4 r4 = *reinterpret_cast<const float4*>(r + e);
+      gv[0] = g4.x; gv[1] = g4.y; gv[2] = g4.z; gv[3] = g4.w;
+      rv[0] = r4.x; rv[1] = r4.y; rv[2] = r4.z; rv[3] = r4.w;
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        gv[c] = e + c < n ? g[e + c] : 0.f;
+        rv[c] = e + c < n ? r[e + c] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const float a = rv[c] + gv[c];
+      uint32_t k = 0;
+      float nr = a;
+      if (a > tau) { nr = a - tau; k = 1u; }
+      else if (a < -tau) { nr = a + tau; k = 3u; }
+      rv[c] = nr;
+      code |= k << (2 * (grp * 4 + c));
+    }
+    if (ALIGNED && e + 3 < n) {
+      *reinterpret_cast<float4*>(r + e) = make_float4(rv[0], rv[1], rv[2], rv[3]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (e + c < n) r[e + c] = rv[c];
+    }
+  }
+  codes[(int64_t)blockIdx.x * TPB + threadIdx.x] = code;
+  int cnt = __popc(code & 0x55555555u);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) tile_count[blockIdx.x] = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+}
+
+// Exclusive prefix of tile counts (in place) and the total, one block.
+__global__ __launch_bounds__(1024) void gtc_scan(int32_t* __restrict__ tile_count, int64_t ntiles,
+                                                 int64_t* __restrict__ total) {
+  __shared__ int64_t part[1024];
+  const int t = threadIdx.x;
+  const int64_t per = (ntiles + 1023) / 1024;
+  const int64_t lo = t * per, hi = lo + per < ntiles ? lo + per : ntiles;
+  int64_t s = 0;
+  for (int64_t i = lo; i < hi; ++i) s += tile_count[i];
+  part[t] = s;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {  // Hillis-Steele inclusive scan
+    int64_t v = t >= o ? part[t - o] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  int64_t run = part[t] - s;  // exclusive
+  for (int64_t i = lo; i < hi; ++i) {
+    const int32_t c = tile_count[i];
+    tile_count[i] = (int32_t)run;
+    run += c;
+  }
+  if (t == 1023) *total = part[1023];
+}
+
+__global__ __launch_bounds__(TPB) void gtc_compact(int64_t n, const uint32_t* __restrict__ codes,
+                                                   const int32_t* __restrict__ tile_off,
+                                                   uint32_t* __restrict__ words) {
+  __shared__ uint64_t wtot[TPB / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t code = codes[(int64_t)blockIdx.x * TPB + threadIdx.x];
+  // per-group counts packed in 16-bit fields: field grp = sent items of group grp
+  uint64_t mine = 0;
+#pragma unroll
+  for (int grp = 0; grp < 4; ++grp)
+    mine |= (uint64_t)__popc((code >> (8 * grp)) & 0x55u) << (16 * grp);
+  // inclusive wave scan
+  uint64_t inc = mine;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint64_t v = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += v;
+  }
+  if (lane == 63) wtot[wave] = inc;
+  __syncthreads();
+  uint64_t before = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < TPB / 64; ++w) {
+    if (w < wave) before += wtot[w];
+    total += wtot[w];
+  }
+  const uint64_t excl = before + inc - mine;  // sent items in earlier threads, per group
+  int64_t pos = tile_off[blockIdx.x];
+  const int64_t base = (int64_t)blockIdx.x * TILE;
+#pragma unroll
+  for (int grp = 0; grp < 4; ++grp) {
+    int64_t p = pos + (int64_t)((excl >> (16 * grp)) & 0xFFFFu);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t k = (code >> (2 * (grp * 4 + c))) & 3u;
+      if (k & 1u) {
+        const uint32_t e = (uint32_t)(base + grp * 1024 + threadIdx.x * 4 + c);
+        words[p++] = (e << 1) | (k >> 1);
+      }
+    }
+    pos += (int64_t)((total >> (16 * grp)) & 0xFFFFu);
+  }
+}
+
+__device__ __forceinline__ int64_t lower_bound_words(const uint32_t* w, int64_t cnt, uint32_t key) {
+  int64_t lo = 0, hi = cnt;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (w[mid] < key) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+template <bool ACC>
+__global__ __launch_bounds__(TPB) void gtc_decode_tiles(const uint32_t* __restrict__ words,
+                                                        const int64_t* __restrict__ count,
+                                                        int64_t capacity, float tau, int64_t n,
+                                                        float* __restrict__ dense) {
+  __shared__ float tile[TILE];
+  __shared__ int64_t range[2];
+  const int64_t base = (int64_t)blockIdx.x * TILE;
+  const int64_t len = n - base < TILE ? n - base : TILE;
+  if (threadIdx.x < 2) {
+    int64_t cnt = *count;
+    cnt = cnt < 0 ? 0 : (cnt > capacity ? capacity : cnt);
+    const int64_t end = base + (threadIdx.x ? len : 0);
+    range[threadIdx.x] = lower_bound_words(words, cnt, (uint32_t)(end << 1));
+  }
+  for (int i = threadIdx.x; i < TILE; i += TPB)
+    tile[i] = (ACC && i < len) ? dense[base + i] : 0.f;
+  __syncthreads();
+  const int64_t lo = range[0], hi = range[1];
+  for (int64_t w = lo + threadIdx.x; w < hi; w += TPB) {
+    const uint32_t word = words[w];
+    const int i = (int)((word >> 1) - (uint32_t)base);
+    const float v = (word & 1u) ? -tau : tau;
+    if ((unsigned)i >= (unsigned)len) continue;  // only for unsorted input
+    if (ACC) tile[i] = tile[i] + v; else tile[i] = v;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < len; i += TPB) dense[base + i] = tile[i];
+}
+
+}  // namespace
+
+int64_t gtc_tiles(int64_t n) { return (n + TILE - 1) / TILE; }
+
+hipError_t gtc_encode(int64_t n, const float* g, float* r, float tau, uint32_t* words,
+                      int64_t* count, uint32_t* ws_codes, int32_t* ws_tile, hipStream_t s) {
+  const int64_t ntiles = gtc_tiles(n);
+  if (ntiles > 0) {
+    const bool aligned = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(r)) & 15) == 0;
+    if (aligned)
+      hipLaunchKernelGGL(gtc_update<true>, dim3((unsigned)ntiles), dim3(TPB), 0, s, n, g, r, tau,
+                         ws_codes, ws_tile);
+    else
+      hipLaunchKernelGGL(gtc_update<false>, dim3((unsigned)ntiles), dim3(TPB), 0, s, n, g, r, tau,
+                         ws_codes, ws_tile);
+  }
+  hipLaunchKernelGGL(gtc_scan, dim3(1), dim3(1024), 0, s, ws_tile, ntiles, count);
+  if (ntiles > 0)
+    hipLaunchKernelGGL(gtc_compact, dim3((unsigned)ntiles), dim3(TPB), 0, s, n, ws_codes, ws_tile,
+                       words);
+  return hipGetLastError();
+}
+
+hipError_t gtc_decode(const uint32_t* words, const int64_t* count, int64_t capacity, float tau,
+                      int64_t n, float* dense, bool accumulate, hipStream_t s) {
+  const int64_t ntiles = gtc_tiles(n);
+  if (ntiles == 0) return hipSuccess;
+  if (accumulate)
+    hipLaunchKernelGGL(gtc_decode_tiles<true>, dim3((unsigned)ntiles), dim3(TPB), 0, s, words,
+                       count, capacity, tau, n, dense);
+  else
+    hipLaunchKernelGGL(gtc_decode_tiles<false>, dim3((unsigned)ntiles), dim3(TPB), 0, s, words,
+                       count, capacity, tau, n, dense);
+  return hipGetLastError();
+}
+
+}  // namespace am

@@ -1,0 +1,212 @@
+// One time step of one LSTM layer, forward and backward, with the recurrent
+// product fused to the cell arithmetic.
+//
+// Work split (both directions): a 256-thread workgroup owns 16 hidden units
+// j0..j0+15 and 64 consecutive active sequences of the step.  The recurrent
+// product's k-range is split across the four waves (k-steps w, w+4, ...), so
+// each wave streams a disjoint quarter of the operands straight from global
+// memory into MFMA fragments; the four partial tiles are summed in LDS in a
+// fixed order (deterministic), and each wave then finishes 16 of the 64 rows.
+// In the 16x16 MFMA output layout a lane holds one unit for four rows; the
+// forward product keeps the four gate tiles (i, f, g, o) of the same units
+// side by side, so every lane has all four gate pre-activations of its
+// (row, unit) pairs in registers and the cell update needs no exchange.
+//
+// Forward  (per active row b, unit j):
+//   a = P[b] + h_{t-1}[b] Wh^T;  i,f,o = sigm, g = tanh;  c = f c_{t-1} + i g;
+//   h = o tanh(c).  Stores h_t, c_t, the gate activations and a copy of h_{t-1}.
+// Backward (reverse time):
+//   dh = dH_above + dA_{t+1} Wh (rows still active at t+1);
+//   do = dh tanh c;  dc = dh o (1 - tanh^2 c) + dc_{t+1};
+//   di = dc g, dg = dc i, df = dc c_{t-1};  dc_t = dc f;
+//   dA = [di i(1-i), df f(1-f), dg (1-g^2), do o(1-o)].
+#include "am_device.h"
+#include "am_internal.h"
+
+namespace am {
+namespace {
+
+constexpr int UNITS = 16;  // hidden units per workgroup
+constexpr int ROWS = 64;   // active sequences per workgroup
+
+template <typename T>
+__global__ __launch_bounds__(256) void lstm_fwd_step_kernel(
+    const T* __restrict__ P, const T* __restrict__ Wh, const T* __restrict__ hprev,
+    const float* __restrict__ cprev, T* __restrict__ Hout, T* __restrict__ Hs,
+    float* __restrict__ Cout, T* __restrict__ G, int nb, int H) {
+  __shared__ f32x4_t red[4][4][4][64];  // [wave][row tile][gate][lane], 64 KB
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j0 = blockIdx.x * UNITS;
+  const int b0 = blockIdx.y * ROWS;
+  const int ksteps = (H + 31) / 32;
+  const int koct = (lane >> 4) * 8;
+
+  f32x4_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) acc[i][g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  if (hprev) {
+    for (int ks = wave; ks < ksteps; ks += 4) {
+      const int k = ks * 32 + koct;
+      const bool kin = k < H;
+      Frag<T> a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = b0 + i * 16 + (lane & 15);
+        a[i] = (kin && row < nb) ? frag_load<T>(hprev + (int64_t)row * H + k) : frag_zero<T>();
+      }
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int wrow = g * H + j0 + (lane & 15);
+        b[g] = kin ? frag_load<T>(Wh + (int64_t)wrow * H + k) : frag_zero<T>();
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) mma_16x16x32(acc[i][g], a[i], b[g]);
+    }
+  }
+
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) red[wave][i][g][lane] = acc[i][g];
+  __syncthreads();
+
+  f32x4_t s[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    s[g] = red[0][wave][g][lane];
+    s[g] += red[1][wave][g][lane];
+    s[g] += red[2][wave][g][lane];
+    s[g] += red[3][wave][g][lane];
+  }
+
+  const int j = j0 + mfma_col(lane);
+  const int G4 = 4 * H;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int row = b0 + wave * 16 + mfma_row(lane, r);
+    if (row >= nb) continue;
+    const T* prow = P + (int64_t)row * G4;
+    const float ai = s[0][r] + to_f32<T>(prow[j]);
+    const float af = s[1][r] + to_f32<T>(prow[H + j]);
+    const float ag = s[2][r] + to_f32<T>(prow[2 * H + j]);
+    const float ao = s[3][r] + to_f32<T>(prow[3 * H + j]);
+    const float gi = sigm(ai), gf = sigm(af), gg = tanh_f(ag), go = sigm(ao);
+    const float cp = cprev ? cprev[(int64_t)row * H + j] : 0.f;
+    const float c = gf * cp + gi * gg;
+    const float h = go * tanh_f(c);
+    const int64_t o = (int64_t)row * H + j;
+    Cout[o] = c;
+    Hout[o] = from_f32<T>(h);
+    Hs[o] = hprev ? hprev[o] : from_f32<T>(0.f);
+    T* grow = G + (int64_t)row * G4;
+    grow[j] = from_f32<T>(gi);
+    grow[H + j] = from_f32<T>(gf);
+    grow[2 * H + j] = from_f32<T>(gg);
+    grow[3 * H + j] = from_f32<T>(go);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void lstm_bwd_step_kernel(
+    const T* __restrict__ dAnext, int nbn, const T* __restrict__ WhT,
+    const T* __restrict__ dHa, const T* __restrict__ G, const float* __restrict__ C,
+    const float* __restrict__ Cprev, float* __restrict__ dc, T* __restrict__ dA, int nb, int H) {
+  __shared__ f32x4_t red[4][4][64];  // [wave][row tile][lane], 16 KB
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j0 = blockIdx.x * UNITS;
+  const int b0 = blockIdx.y * ROWS;
+  const int G4 = 4 * H;
+  const int ksteps = G4 / 32;  // 4H is a multiple of 32 when H % 8 == 0
+  const int koct = (lane >> 4) * 8;
+
+  f32x4_t acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  if (dAnext && b0 < nbn) {
+    for (int ks = wave; ks < ksteps; ks += 4) {
+      const int k = ks * 32 + koct;
+      Frag<T> a[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = b0 + i * 16 + (lane & 15);
+        a[i] = row < nbn ? frag_load<T>(dAnext + (int64_t)row * G4 + k) : frag_zero<T>();
+      }
+      const Frag<T> b = frag_load<T>(WhT + (int64_t)(j0 + (lane & 15)) * G4 + k);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mma_16x16x32(acc[i], a[i], b);
+    }
+  }
+
+#pragma unroll
+  for (int i = 0; i < 4; ++i) red[wave][i][lane] = acc[i];
+  __syncthreads();
+  f32x4_t s = red[0][wave][lane];
+  s += red[1][wave][lane];
+  s += red[2][wave][lane];
+  s += red[3][wave][lane];
+
+  const int j = j0 + mfma_col(lane);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int row = b0 + wave * 16 + mfma_row(lane, r);
+    if (row >= nb) continue;
+    const int64_t o = (int64_t)row * H + j;
+    const T* grow = G + (int64_t)row * G4;
+    const float gi = to_f32<T>(grow[j]), gf = to_f32<T>(grow[H + j]);
+    const float gg = to_f32<T>(grow[2 * H + j]), go = to_f32<T>(grow[3 * H + j]);
+    const float c = C[o];
+    const float cp = Cprev ? Cprev[o] : 0.f;
+    const float dcn = row < nbn ? dc[o] : 0.f;
+    const float dh = to_f32<T>(dHa[o]) + s[r];
+    const float tc = tanh_f(c);
+    const float d_o = dh * tc;
+    const float dcell = dh * go * (1.f - tc * tc) + dcn;
+    const float d_i = dcell * gg, d_g = dcell * gi, d_f = dcell * cp;
+    dc[o] = dcell * gf;
+    T* arow = dA + (int64_t)row * G4;
+    arow[j] = from_f32<T>(d_i * gi * (1.f - gi));
+    arow[H + j] = from_f32<T>(d_f * gf * (1.f - gf));
+    arow[2 * H + j] = from_f32<T>(d_g * (1.f - gg * gg));
+    arow[3 * H + j] = from_f32<T>(d_o * go * (1.f - go));
+  }
+}
+
+}  // namespace
+
+hipError_t lstm_fwd_step(const LstmFwdStep& a, hipStream_t s) {
+  if (a.nb <= 0) return hipSuccess;
+  dim3 grid(a.hidden / UNITS, (a.nb + ROWS - 1) / ROWS);
+  if (a.bf16)
+    hipLaunchKernelGGL(lstm_fwd_step_kernel<bf16_t>, grid, dim3(256), 0, s,
+                       (const bf16_t*)a.P, (const bf16_t*)a.Wh, (const bf16_t*)a.hprev, a.cprev,
+                       (bf16_t*)a.H, (bf16_t*)a.Hs, a.C, (bf16_t*)a.G, a.nb, a.hidden);
+  else
+    hipLaunchKernelGGL(lstm_fwd_step_kernel<float>, grid, dim3(256), 0, s,
+                       (const float*)a.P, (const float*)a.Wh, (const float*)a.hprev, a.cprev,
+                       (float*)a.H, (float*)a.Hs, a.C, (float*)a.G, a.nb, a.hidden);
+  return hipGetLastError();
+}
+
+hipError_t lstm_bwd_step(const LstmBwdStep& a, hipStream_t s) {
+  if (a.nb <= 0) return hipSuccess;
+  dim3 grid(a.hidden / UNITS, (a.nb + ROWS - 1) / ROWS);
+  if (a.bf16)
+    hipLaunchKernelGGL(lstm_bwd_step_kernel<bf16_t>, grid, dim3(256), 0, s,
+                       (const bf16_t*)a.dAnext, a.nbn, (const bf16_t*)a.WhT, (const bf16_t*)a.dHa,
+                       (const bf16_t*)a.G, a.C, a.Cprev, a.dc, (bf16_t*)a.dA, a.nb, a.hidden);
+  else
+    hipLaunchKernelGGL(lstm_bwd_step_kernel<float>, grid, dim3(256), 0, s,
+                       (const float*)a.dAnext, a.nbn, (const float*)a.WhT, (const float*)a.dHa,
+                       (const float*)a.G, a.C, a.Cprev, a.dc, (float*)a.dA, a.nb, a.hidden);
+  return hipGetLastError();
+}
+
+}  // namespace am

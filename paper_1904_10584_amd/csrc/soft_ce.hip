@@ -1,0 +1,196 @@
+// Sparse soft-target cross-entropy (student-teacher training against the
+// teacher's k-best posteriors), HBM-bound.
+//
+// One wave per frame row: the row of logits is read once with 16-byte loads
+// and kept in registers (up to 8192 classes), max and sum-of-exponentials are
+// wave reductions, the k teacher logits are read with wave-uniform loads, and
+// the gradient row  s (M softmax(z) - scatter(p))  is written once.  A teacher
+// entry is subtracted by the one lane that holds its class; which register
+// holds it is a wave-uniform choice, taken with uniform branches.  Row losses
+// are summed per block in a fixed order, then over blocks by a single block,
+// so the loss is deterministic.
+#include "am_device.h"
+#include "am_internal.h"
+
+namespace am {
+namespace {
+
+constexpr int ROWS_PER_BLOCK = 4;  // one per wave
+
+template <typename DT> __device__ __forceinline__ void store4(DT* p, float4 v);
+template <> __device__ __forceinline__ void store4<float>(float* p, float4 v) {
+  *reinterpret_cast<float4*>(p) = v;
+}
+template <> __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float4 v) {
+  uint2 w;
+  w.x = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+  w.y = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+  *reinterpret_cast<uint2*>(p) = w;
+}
+
+template <int NCH, typename DT>
+__global__ __launch_bounds__(256) void soft_ce_rows(
+    int64_t N, int C, int K, const float* __restrict__ z, const int32_t* __restrict__ idx,
+    const float* __restrict__ prob, const uint8_t* __restrict__ mask,
+    const float* __restrict__ scale_dev, float scale_host, DT* __restrict__ dz,
+    float* __restrict__ partials) {
+  __shared__ float wl[ROWS_PER_BLOCK];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t f = (int64_t)blockIdx.x * ROWS_PER_BLOCK + wave;
+  float row_loss = 0.f;
+
+  if (f < N) {
+    const float m = mask ? (mask[f] != 0 ? 1.f : 0.f) : 1.f;
+    const float s = m * (scale_dev ? *scale_dev : scale_host);
+    const float* zr = z + f * C;
+    DT* dr = dz + f * C;
+    if (s == 0.f) {
+#pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        const int c = i * 256 + lane * 4;
+        if (c < C) store4<DT>(dr + c, make_float4(0.f, 0.f, 0.f, 0.f));
+      }
+    } else {
+      float4 v[NCH];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        const int c = i * 256 + lane * 4;
+        if (c < C) {
+          v[i] = *reinterpret_cast<const float4*>(zr + c);
+          mx = fmaxf(mx, fmaxf(fmaxf(v[i].x, v[i].y), fmaxf(v[i].z, v[i].w)));
+        } else {
+          v[i] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+        }
+      }
+      mx = wave_max(mx);
+      float se = 0.f;
+#pragma unroll
+      for (int i = 0; i < NCH; ++i)
+        se += __expf(v[i].x - mx) + __expf(v[i].y - mx) + __expf(v[i].z - mx) + __expf(v[i].w - mx);
+      se = wave_sum(se);
+      const float lse = mx + __logf(se);
+
+      const int32_t* ir = idx + f * K;
+      const float* pr = prob + f * K;
+      float mass = 0.f, lf = 0.f;
+      for (int jj = 0; jj < K; ++jj) {
+        const int c = ir[jj];
+        if (c < 0 || c >= C) continue;  // empty slot (or out of range: ignored)
+        const float p = pr[jj];
+        mass += p;
+        lf -= p * (zr[c] - lse);
+      }
+      const float sm = s * mass;
+#pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        v[i].x = sm * __expf(v[i].x - lse);
+        v[i].y = sm * __expf(v[i].y - lse);
+        v[i].z = sm * __expf(v[i].z - lse);
+        v[i].w = sm * __expf(v[i].w - lse);
+      }
+      for (int jj = 0; jj < K; ++jj) {
+        const int c = ir[jj];
+        if (c < 0 || c >= C) continue;
+        const int ci = c >> 8, owner = (c & 255) >> 2, cc = c & 3;
+        const float d = lane == owner ? s * pr[jj] : 0.f;
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+          if (i == ci) {  // wave-uniform
+            v[i].x -= cc == 0 ? d : 0.f;
+            v[i].y -= cc == 1 ? d : 0.f;
+            v[i].z -= cc == 2 ? d : 0.f;
+            v[i].w -= cc == 3 ? d : 0.f;
+          }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        const int c = i * 256 + lane * 4;
+        if (c < C) store4<DT>(dr + c, v[i]);
+      }
+      row_loss = s * lf;
+    }
+  }
+  if (lane == 0) wl[wave] = row_loss;
+  __syncthreads();
+  if (threadIdx.x == 0) partials[blockIdx.x] = ((wl[0] + wl[1]) + wl[2]) + wl[3];
+}
+
+// Fixed-order sum of the per-block losses.
+__global__ __launch_bounds__(256) void sum_partials(const float* __restrict__ partials, int64_t n,
+                                                    float* __restrict__ out) {
+  __shared__ float red[256];
+  float acc = 0.f;
+  for (int64_t i = threadIdx.x; i < n; i += 256) acc += partials[i];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = red[0];
+}
+
+// 1 / (number of rows with a nonzero mask), 0 if there are none.
+__global__ __launch_bounds__(256) void mask_scale(const uint8_t* __restrict__ mask, int64_t n,
+                                                  float* __restrict__ out) {
+  __shared__ int64_t red[256];
+  int64_t cnt = 0;
+  for (int64_t i = threadIdx.x; i < n; i += 256) cnt += mask[i] != 0;
+  red[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = red[0] > 0 ? 1.0f / (float)red[0] : 0.f;
+}
+
+template <int NCH, typename DT>
+void launch_rows(const SoftCeArgs& a, const float* scale_dev, float scale_host, hipStream_t s) {
+  const int64_t blocks = (a.N + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK;
+  hipLaunchKernelGGL((soft_ce_rows<NCH, DT>), dim3((unsigned)blocks), dim3(256), 0, s, a.N, a.C,
+                     a.K, a.z, a.idx, a.prob, a.mask, scale_dev, scale_host,
+                     static_cast<DT*>(a.dz), a.ws_partials);
+}
+
+template <typename DT>
+hipError_t dispatch_rows(const SoftCeArgs& a, const float* sd, float sh, hipStream_t s) {
+  const int nch = (a.C + 255) / 256;
+  if (nch <= 2) launch_rows<2, DT>(a, sd, sh, s);
+  else if (nch <= 4) launch_rows<4, DT>(a, sd, sh, s);
+  else if (nch <= 8) launch_rows<8, DT>(a, sd, sh, s);
+  else if (nch <= 12) launch_rows<12, DT>(a, sd, sh, s);
+  else if (nch <= 16) launch_rows<16, DT>(a, sd, sh, s);
+  else if (nch <= 24) launch_rows<24, DT>(a, sd, sh, s);
+  else if (nch <= 32) launch_rows<32, DT>(a, sd, sh, s);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int64_t soft_ce_partials(int64_t N) { return (N + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK; }
+
+hipError_t soft_ce(const SoftCeArgs& a, hipStream_t s) {
+  const float* sd = nullptr;
+  float sh = 1.f;
+  if (a.reduction == 0) {  // mean over valid rows
+    if (a.mask) {
+      hipLaunchKernelGGL(mask_scale, dim3(1), dim3(256), 0, s, a.mask, a.N, a.ws_scale);
+      sd = a.ws_scale;
+    } else {
+      sh = a.N > 0 ? 1.0f / (float)a.N : 0.f;
+    }
+  }
+  hipError_t e = hipSuccess;
+  if (a.N > 0) {
+    e = a.dz_bf16 ? dispatch_rows<bf16_t>(a, sd, sh, s) : dispatch_rows<float>(a, sd, sh, s);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(sum_partials, dim3(1), dim3(256), 0, s, a.ws_partials, a.n_partials, a.loss);
+  return hipGetLastError();
+}
+
+}  // namespace am

@@ -1,0 +1,183 @@
+"""GPU parity of the HBM-bound entry points against the oracle: SGD and the
+bf16 cast (bit-exact), threshold encode/decode (bit-exact) and the sparse
+soft-target cross-entropy (fp32 tolerance).  Calls go through the C ABI."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1904_10584_amd import binding as am
+from tests.gpu_util import rel_l2, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _bits32(a):
+    return np.asarray(a, np.float32).view(np.uint32)
+
+
+@pytest.mark.parametrize("n,offset", [(1, 0), (1003, 0), (1 << 20, 0), (77777, 1)])
+def test_sgd_bit_exact(n, offset):
+    say(f"sgd n={n} offset={offset}")
+    rng = np.random.default_rng(n)
+    w = rng.standard_normal(n + offset).astype(np.float32)
+    u = (rng.standard_normal(n + offset) * 3).astype(np.float32)
+    w[:5] = [0.0, -0.0, 1e-40, 3e38, -1e-45][: min(5, n + offset)]
+    lr = np.float32(0.01)
+    wd = to_dev(w)
+    ud = to_dev(u)
+    bd = torch.zeros(n + offset, dtype=torch.bfloat16, device="cuda")
+    am.sgd_apply(wd[offset:], ud[offset:], lr, bd[offset:])
+    ref_w, ref_b = oracle.sgd_apply(w[offset:], u[offset:], lr)
+    got_w = wd.cpu().numpy()[offset:]
+    got_b = bd.cpu().view(torch.int16).numpy().view(np.uint16)[offset:]
+    np.testing.assert_array_equal(_bits32(got_w), _bits32(ref_w))
+    np.testing.assert_array_equal(got_b, ref_b)
+
+
+def test_cast_bit_exact_special_values():
+    hi = np.arange(1 << 16, dtype=np.uint32) << np.uint32(16)
+    lows = np.array([0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF], dtype=np.uint32)
+    x = (hi[:, None] | lows[None, :]).ravel().view(np.float32)
+    d = torch.empty(x.shape[0], dtype=torch.bfloat16, device="cuda")
+    am.cast_f32_to_bf16(to_dev(x), d)
+    got = d.cpu().view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(got, oracle.bf16_bits(x))
+
+
+def _encode_gpu(g, r, tau, capacity=None):
+    n = g.shape[0]
+    gd, rd = to_dev(g), to_dev(r)
+    words = torch.zeros(max(capacity or n, 1), dtype=torch.int32, device="cuda")
+    count = torch.full((1,), -7, dtype=torch.int64, device="cuda")
+    ws = torch.zeros(max(am.encode_workspace_bytes(n), 256), dtype=torch.uint8, device="cuda")
+    am.grad_threshold_encode(gd, rd, tau, words, count, ws)
+    c = int(count.cpu()[0])
+    return rd.cpu().numpy(), words.cpu().numpy().view(np.uint32)[:c], c, words, count
+
+
+@pytest.mark.parametrize("n", [0, 1, 4095, 4096, 4097, 1_000_003])
+def test_encode_bit_exact(n):
+    say(f"encode n={n}")
+    rng = np.random.default_rng(n + 1)
+    tau = np.float32(1e-3)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    r = (rng.standard_normal(n) * 5e-4).astype(np.float32)
+    ref_r, ref_w, ref_c = oracle.grad_threshold_encode(g, r, tau)
+    got_r, got_w, got_c, _, _ = _encode_gpu(g, r, tau)
+    assert got_c == ref_c
+    np.testing.assert_array_equal(_bits32(got_r), _bits32(ref_r))
+    np.testing.assert_array_equal(got_w, ref_w)
+
+
+def test_encode_adversarial_and_extremes():
+    tau = np.float32(0.5)
+    sub = np.array([1], np.uint32).view(np.float32)[0]
+    base_g = np.array([0.5, -0.5, np.nextafter(np.float32(0.5), np.float32(1)), 1.0, -1.75, -0.0,
+                       sub, np.inf, -np.inf, np.nan, 3e38, 0.0], np.float32)
+    base_r = np.array([0, 0, 0, 0, 0, -0.0, sub, 0, 0, 0, 3e38, 1e-30], np.float32)
+    g = np.tile(base_g, 700)
+    r = np.tile(base_r, 700)
+    ref_r, ref_w, ref_c = oracle.grad_threshold_encode(g, r, tau)
+    got_r, got_w, got_c, _, _ = _encode_gpu(g, r, tau)
+    assert got_c == ref_c
+    np.testing.assert_array_equal(_bits32(got_r), _bits32(ref_r))
+    np.testing.assert_array_equal(got_w, ref_w)
+    # every element sent / none sent
+    for tau2, gg in ((np.float32(1e-3), np.full(9000, 1.0, np.float32)),
+                     (np.float32(np.inf), np.full(9000, 1.0, np.float32))):
+        rr = np.zeros_like(gg)
+        ref_r, ref_w, ref_c = oracle.grad_threshold_encode(gg, rr, tau2)
+        got_r, got_w, got_c, _, _ = _encode_gpu(gg, rr, tau2)
+        assert got_c == ref_c
+        np.testing.assert_array_equal(got_w, ref_w)
+        np.testing.assert_array_equal(_bits32(got_r), _bits32(ref_r))
+
+
+def test_encode_multi_step_residual_feedback():
+    rng = np.random.default_rng(5)
+    n, tau = 300_001, np.float32(2e-3)
+    r = np.zeros(n, np.float32)
+    rd = to_dev(r)
+    words = torch.zeros(n, dtype=torch.int32, device="cuda")
+    count = torch.zeros(1, dtype=torch.int64, device="cuda")
+    ws = torch.zeros(am.encode_workspace_bytes(n), dtype=torch.uint8, device="cuda")
+    for step in range(5):
+        g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+        r, ref_w, ref_c = oracle.grad_threshold_encode(g, r, tau)
+        am.grad_threshold_encode(to_dev(g), rd, tau, words, count, ws)
+        c = int(count.cpu()[0])
+        assert c == ref_c, step
+        np.testing.assert_array_equal(_bits32(rd.cpu().numpy()), _bits32(r))
+        np.testing.assert_array_equal(words.cpu().numpy().view(np.uint32)[:c], ref_w)
+
+
+@pytest.mark.parametrize("accumulate", [False, True])
+@pytest.mark.parametrize("n", [1, 4097, 1_000_003])
+def test_decode_bit_exact(n, accumulate):
+    rng = np.random.default_rng(n)
+    tau = np.float32(1e-3)
+    g = (rng.standard_normal(n) * 1.5e-3).astype(np.float32)
+    r = np.zeros(n, np.float32)
+    _, ref_w, ref_c = oracle.grad_threshold_encode(g, r, tau)
+    _, _, c, words, count = _encode_gpu(g, r, tau)
+    base = rng.standard_normal(n).astype(np.float32)
+    dense = to_dev(base) if accumulate else to_dev(np.full(n, 7.0, np.float32))
+    am.grad_threshold_decode(words, count, tau, dense, accumulate=accumulate)
+    ref = oracle.grad_threshold_decode(ref_w, ref_c, tau, n, dense=base, accumulate=accumulate)
+    np.testing.assert_array_equal(_bits32(dense.cpu().numpy()), _bits32(ref))
+
+
+def _ce_case(N, C, K, seed, empty_slots=False, dup=False, mask=False):
+    rng = np.random.default_rng(seed)
+    z = (rng.standard_normal((N, C)) * 3).astype(np.float32)
+    idx = np.stack([rng.choice(C, K, replace=False) for _ in range(N)]).astype(np.int32)
+    prob = (rng.dirichlet(np.full(K, 0.3), size=N) * 0.95).astype(np.float32)
+    if empty_slots and K > 1:
+        idx[::3, -1] = -1
+    if dup and K > 1:
+        idx[::5, 1] = idx[::5, 0]
+    m = (rng.random(N) > 0.3).astype(np.uint8) if mask else None
+    return z, idx, prob, m
+
+
+@pytest.mark.parametrize("N,C,K,opts", [
+    (1, 4, 1, {}), (37, 500, 5, {"empty_slots": True}), (1000, 3000, 20, {"dup": True}),
+    (130, 8192, 20, {"mask": True}), (257, 6000, 1, {}), (64, 260, 3, {"mask": True, "empty_slots": True}),
+])
+@pytest.mark.parametrize("dz_bf16", [False, True])
+@pytest.mark.parametrize("reduction", [am.MEAN_VALID, am.SUM])
+def test_soft_ce_matches_oracle(N, C, K, opts, dz_bf16, reduction):
+    say(f"soft_ce N={N} C={C} K={K} {opts} bf16={dz_bf16} red={reduction}")
+    z, idx, prob, m = _ce_case(N, C, K, seed=N + C, **opts)
+    ref_loss, ref_dz = oracle.sparse_soft_ce(z, idx, prob, m, reduction)
+    dz = torch.empty((N, C), dtype=torch.bfloat16 if dz_bf16 else torch.float32, device="cuda")
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    ws = torch.empty(am.ce_workspace_bytes(N), dtype=torch.uint8, device="cuda")
+    am.sparse_soft_ce(to_dev(z), to_dev(idx), to_dev(prob), loss, dz, ws,
+                      mask=to_dev(m) if m is not None else None, reduction=reduction)
+    got_loss = float(loss.cpu()[0])
+    got_dz = dz.float().cpu().numpy()
+    assert abs(got_loss - ref_loss) <= 1e-5 * abs(ref_loss) + 1e-7
+    tol = 4e-3 if dz_bf16 else 1e-5
+    assert rel_l2(got_dz, ref_dz) <= tol
+    if m is not None:
+        assert np.all(got_dz[m == 0] == 0.0)
+
+
+def test_soft_ce_masked_rows_not_read():
+    N, C, K = 40, 512, 4
+    z, idx, prob, _ = _ce_case(N, C, K, seed=3)
+    m = np.ones(N, np.uint8)
+    m[5:9] = 0
+    z_poison = z.copy()
+    z_poison[5:9] = np.nan
+    ref_loss, ref_dz = oracle.sparse_soft_ce(z, idx, prob, m)
+    dz = torch.empty((N, C), dtype=torch.float32, device="cuda")
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    ws = torch.empty(am.ce_workspace_bytes(N), dtype=torch.uint8, device="cuda")
+    am.sparse_soft_ce(to_dev(z_poison), to_dev(idx), to_dev(prob), loss, dz, ws, mask=to_dev(m))
+    assert np.isfinite(float(loss.cpu()[0]))
+    assert abs(float(loss.cpu()[0]) - ref_loss) <= 1e-5 * abs(ref_loss)
+    assert np.all(np.isfinite(dz.cpu().numpy()))
