@@ -1,0 +1,239 @@
+"""Benchmark of one GPU's student training step.
+
+A step is the whole hot path on one batch: LSTM forward, sparse soft-target
+cross-entropy, BPTT, threshold encode of the full gradient with residual
+error feedback, decode, and SGD on the fp32 master weights with a fresh bf16
+copy.  Default workload: 5 LSTM layers x 768 cells, 192-dim input, 3000
+senones, 256 chunks x 64 frames, k = 20 teacher targets, bf16 weights and
+activations with fp32 masters (synthetic, seeded inputs).
+
+Prints one JSON line: frames/s over the timed steps, the roofline of the
+kernel class that takes the most time (its average launch duration measured
+with HIP events over the timed steps), and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X dense fp32 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "training frames/sec on 1 MI355X (5x768 LSTM, 3000 senones); MFMA util %"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="paper-5x768")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-chunks", type=int, default=0,
+                    help="chunks the CPU oracle runs forward/backward on (0 = the whole batch)")
+    return ap.parse_args()
+
+
+def kernel_sources_digest(names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_1904_10584_amd", "csrc", n), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(kclass, per_launch_units):
+    """HBM bytes per launch from a committed counter summary, if it still
+    matches the kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        table = json.load(fh)
+    ent = table.get(kclass)
+    if not ent:
+        return None
+    if ent.get("sources_sha") != kernel_sources_digest(ent["sources"]):
+        return None
+    return ent["hbm_bytes_per_launch"]
+
+
+def make_step(wl, am, synth, trainer):
+    import torch
+    w = synth.WORKLOADS[wl]
+    dtype = am.BF16 if w["dtype"] == "bf16" else am.F32
+    m = am.Model(w["layers"], w["input_dim"], w["hidden"], w["classes"], dtype)
+    lengths = None
+    if "len_lo" in w:
+        lengths = synth.utterance_lengths(w["B"], w["len_lo"], w["len_hi"])
+        T = int(lengths[0])
+    else:
+        T = w["T"]
+    st = trainer.StudentStep(m, T, w["B"], w["K"], lengths=lengths, lr=w["lr"], tau=w["tau"], gtc=True)
+    n = st.n
+    st.load_params(torch.from_numpy(synth.init_params(n, w["hidden"])).cuda())
+    x = synth.features(st.N, w["input_dim"])
+    idx, prob = synth.teacher_targets(st.N, w["classes"], w["K"], w["mass"],
+                                      one_hot_frac=w.get("one_hot_frac", 0.0))
+    st.load_batch(torch.from_numpy(x).cuda(), torch.from_numpy(idx).cuda(),
+                  torch.from_numpy(prob).cuda())
+    torch.cuda.synchronize()
+    return st, w, T, lengths
+
+
+def step_flops(w, T, lengths):
+    """Algorithmic flops of forward + backward: 6 flops per weight per frame
+    (2 forward, 4 backward) except that the input gradient of layer 0 is not
+    formed.  Recurrent products are skipped at each sequence's first frame
+    only in the backward (no dA_{t+1}); counted as dense here."""
+    L, D, H, C = w["layers"], w["input_dim"], w["hidden"], w["classes"]
+    N = T * w["B"] if lengths is None else int(sum(lengths))
+    G = 4 * H
+    per_frame = 0
+    for l in range(L):
+        Dl = D if l == 0 else H
+        per_frame += 2 * G * (Dl + H)              # forward products
+        per_frame += 2 * G * (Dl + H)              # weight gradients
+        per_frame += 2 * G * H                     # recurrent data gradient
+        if l > 0:
+            per_frame += 2 * G * Dl                # input data gradient
+    per_frame += 3 * 2 * C * H                     # output layer fwd, dW, dH
+    return per_frame * N, N
+
+
+def cpu_baseline(wl, synth, chunks):
+    """The oracle, as it stands, on a bounded sample: forward, CE and BPTT on
+    `chunks` chunks of the batch, plus encode, decode and SGD of the whole
+    flat gradient; scaled to frames/s of a full step."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:
+        threads = 1
+    w = synth.WORKLOADS[wl]
+    d = oracle.ModelDims(w["layers"], w["input_dim"], w["hidden"], w["classes"])
+    n = oracle.param_count(d)
+    master = synth.init_params(n, d.hidden)
+    T, B = w["T"], w["B"]
+    S = B if chunks <= 0 else min(chunks, B)
+    x = synth.features(T * S, d.input_dim)
+    idx, prob = synth.teacher_targets(T * S, d.classes, w["K"], w["mass"])
+    p = oracle.bf16_round(master) if w["dtype"] == "bf16" else master
+    xe = oracle.bf16_round(x) if w["dtype"] == "bf16" else x
+    t0 = time.perf_counter()
+    logits, cache = oracle.lstm_am_forward(p, d, xe, T, S)
+    loss, dz = oracle.sparse_soft_ce(logits, idx, prob)
+    g = oracle.lstm_am_backward(p, d, cache, dz)
+    t1 = time.perf_counter()
+    r, words, count = oracle.grad_threshold_encode(g.astype(np.float32), np.zeros(n, np.float32), w["tau"])
+    u = oracle.grad_threshold_decode(words, count, w["tau"], n)
+    oracle.sgd_apply(master, u, w["lr"])
+    t2 = time.perf_counter()
+    step_s = (t1 - t0) * (B / S) + (t2 - t1)
+    return {"value": round(T * B / step_s, 2), "unit": "frames/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"fp64 numpy oracle: forward+CE+BPTT on {S} of {B} chunks x {T} frames "
+                       f"({t1 - t0:.1f} s, scaled x{B / S:g}) plus encode/decode/SGD of all "
+                       f"{n} parameters ({t2 - t1:.1f} s)")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    from paper_1904_10584_amd import binding as am
+    from paper_1904_10584_amd import synth, trainer
+
+    torch.cuda.set_device(0)
+    st, w, T, lengths = make_step(args.workload, am, synth, trainer)
+
+    # warm-up, then one recorded step with every kernel class to find the
+    # class that takes the most time
+    for _ in range(args.warmup):
+        st.step()
+    torch.cuda.synchronize()
+    am.profile_begin(range(10))
+    st.step()
+    am.profile_end()
+    totals = {k: am.profile_get(k) for k in range(10)}
+    dom = max(range(10), key=lambda k: totals[k]["ms"])
+    torch.cuda.synchronize()
+
+    # timed steps; the dominant class is bracketed by HIP events on its stream
+    am.profile_begin([dom])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        st.step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    am.profile_end()
+    kt = am.profile_get(dom)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    flops, N = step_flops(w, T, lengths)
+    frames_per_s = N / (ms_per_step * 1e-3)
+
+    avg_ms = kt["ms"] / max(kt["launches"], 1)
+    name = am.KERNEL_CLASSES[dom]
+    hbm_classes = {am.K_CE, am.K_ENCODE, am.K_DECODE, am.K_SGD, am.K_MISC}
+    bf16 = w["dtype"] == "bf16"
+    if dom in hbm_classes:
+        per_launch = kt["bytes"] / max(kt["launches"], 1)
+        achieved = per_launch / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    else:
+        per_launch = kt["flops"] / max(kt["launches"], 1)
+        achieved = per_launch / (avg_ms * 1e-3) / 1e12
+        peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = traffic_for(name, per_launch)
+    roof["kernel"] = name
+    roof["launches_per_step"] = kt["launches"] // args.steps
+    roof["avg_launch_us"] = round(avg_ms * 1e3, 2)
+    roof["algorithmic_per_launch"] = per_launch
+
+    out = {
+        "metric": METRIC,
+        "value": round(frames_per_s, 1),
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "layers": w["layers"], "hidden": w["hidden"],
+                   "input_dim": w["input_dim"], "classes": w["classes"], "chunks": w["B"],
+                   "frames_per_chunk": T if lengths is None else None,
+                   "frames_per_step": N, "k": w["K"], "tau": w["tau"], "lr": w["lr"],
+                   "step": "forward+soft_ce+bptt+threshold_encode+decode+sgd",
+                   "parallelism": "single-gpu"},
+        "mfma_util_pct": round(100.0 * flops / (ms_per_step * 1e-3) / (
+            (PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS) * 1e12), 2),
+        "step_tflop": round(flops / 1e12, 4),
+        "roofline": roof,
+        "kernel_ms_per_step": {am.KERNEL_CLASSES[k]: round(totals[k]["ms"], 3) for k in range(10)},
+    }
+    if not args.no_cpu_baseline and args.workload in ("paper-5x768", "tiny-2x64", "wide-5x1536"):
+        out["cpu_baseline"] = cpu_baseline(args.workload, synth, args.cpu_chunks)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
