@@ -83,8 +83,14 @@ __device__ __forceinline__ void mma_16x16x32(f32x4_t& acc, const Frag<float>& a,
 __device__ __forceinline__ int mfma_row(int lane, int r) { return 4 * (lane >> 4) + r; }
 __device__ __forceinline__ int mfma_col(int lane) { return lane & 15; }
 
-__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
-__device__ __forceinline__ float tanh_f(float x) { return tanhf(x); }
+// Logistic sigmoid and tanh from their definitions with the hardware
+// exponential and reciprocal (about 1e-7 absolute error):
+//   sigm(x) = 1 / (1 + e^-x),   tanh(x) = 2 sigm(2x) - 1.
+// Both saturate correctly: e^-x overflows to +inf and its reciprocal is 0.
+__device__ __forceinline__ float sigm(float x) {
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-x));
+}
+__device__ __forceinline__ float tanh_f(float x) { return 2.0f * sigm(2.0f * x) - 1.0f; }
 
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll

@@ -13,13 +13,21 @@ namespace am {
 // bias is per column, input type.  Requirements (checked by the caller):
 // 16-byte aligned rows; a k-major K and an m/n-major M or N that is a
 // multiple of 8 (bf16) / 4 (fp32).
+// Optional (m/n-major B only): columns n >= n_split of B come from B2
+// (row stride ldb2) and the matching columns of C go to C2 (ldc2).
+// Optional (m-major A only): rowsum[m] = sum_k A(m,k) in fp32.
+// Optional: ws/ws_floats, fp32 scratch that lets a TN product split K.
 struct GemmArgs {
-  const void* A; int64_t lda; bool a_kmajor;
-  const void* B; int64_t ldb; bool b_kmajor;
-  void* C; int64_t ldc; bool c_f32;
-  const void* bias;
-  int M, N, K;
-  bool bf16;
+  const void* A = nullptr; int64_t lda = 0; bool a_kmajor = true;
+  const void* B = nullptr; int64_t ldb = 0; bool b_kmajor = true;
+  const void* B2 = nullptr; int64_t ldb2 = 0; int n_split = 0;
+  void* C = nullptr; int64_t ldc = 0; bool c_f32 = false;
+  void* C2 = nullptr; int64_t ldc2 = 0;
+  const void* bias = nullptr;
+  float* rowsum = nullptr;
+  int M = 0, N = 0, K = 0;
+  bool bf16 = false;
+  float* ws = nullptr; int64_t ws_floats = 0;
 };
 hipError_t gemm(const GemmArgs& g, hipStream_t s);
 
@@ -56,6 +64,43 @@ struct LstmBwdStep {
   bool bf16;
 };
 hipError_t lstm_bwd_step(const LstmBwdStep& a, hipStream_t s);
+
+// Persistent layer kernels (all time steps in one cooperative launch).
+// The schedule of a batch: T steps, B sequences, N frames; with varlen the
+// sorted lengths (B <= 1024), else every sequence has T frames.
+struct PersistSchedule {
+  int T, B, N;
+  int varlen;
+  uint16_t lens[1024];
+};
+struct PersistFwd {
+  const void* P;       // [N][4H] input projections (+ bias)
+  const void* Wh;      // [4H][H]
+  const void* h0;      // [B][H] initial h (activation type) or null (zero)
+  const float* c0;     // [B][H] initial c
+  void* H; void* Hs; float* C; void* G;  // [N][H], [N][H], [N][H], [N][4H] (written)
+  unsigned* counters;  // one per block of 64 sequences, zero at launch
+  int* err;            // set to 1 if a step barrier timed out
+  int hidden;
+};
+struct PersistBwd {
+  const void* Wh;      // [4H][H]
+  const void* dHa;     // [N][H] gradient from the layer above
+  const void* G;       // [N][4H]
+  const float* C;      // [N][H]
+  const float* c0;     // [B][H]
+  void* dA;            // [N][4H] (written)
+  unsigned* counters;
+  int* err;
+  int hidden;
+};
+// Whether the persistent kernel covers this shape and its grid can be
+// resident at once on the current device.
+bool lstm_persistent_fits(bool forward, int hidden, int B, bool bf16, int T);
+// *used is false (and nothing is launched) when the grid cannot be resident
+// at once or the shape is not covered; the caller then runs single steps.
+hipError_t lstm_fwd_persistent(PersistFwd a, PersistSchedule ps, bool bf16, hipStream_t s, bool* used);
+hipError_t lstm_bwd_persistent(PersistBwd a, PersistSchedule ps, bool bf16, hipStream_t s, bool* used);
 
 // Sparse soft-target cross-entropy rows (see sparse_soft_ce in the C ABI).
 struct SoftCeArgs {

@@ -164,11 +164,32 @@ am_status make_schedule(int32_t T, int32_t B, const int32_t* lengths, Schedule& 
   return AM_OK;
 }
 
+// The persistent layer kernels are used when they fit; AM_STEP_KERNELS=1 in
+// the environment forces one launch per time step instead.
+bool persistent_enabled() {
+  const char* v = getenv("AM_STEP_KERNELS");
+  return !(v && v[0] && v[0] != '0');
+}
+
+am::PersistSchedule persist_schedule(const Schedule& sc) {
+  am::PersistSchedule ps;
+  ps.T = sc.T;
+  ps.B = sc.B;
+  ps.N = (int)sc.N;
+  ps.varlen = 0;
+  for (int b = 0; b < sc.B; ++b)
+    if (sc.lens[b] != sc.T) ps.varlen = 1;
+  memset(ps.lens, 0, sizeof ps.lens);
+  if (ps.varlen)
+    for (int b = 0; b < sc.B; ++b) ps.lens[b] = (uint16_t)sc.lens[b];
+  return ps;
+}
+
 // Workspace carve-up (256-byte aligned regions).
 struct WsLayout {
   std::vector<int64_t> h, hs, c, g;  // per layer
-  int64_t p_da, dh, wht, dc, c0, h0, colsum, total;
-  static constexpr int COLSUM_CHUNKS = 64;
+  int64_t p_da, dh, wht, dc, c0, h0, splitk, splitk_floats, sync, total;
+  static constexpr int MAX_SPLITS = 8;
 };
 
 int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
@@ -190,8 +211,16 @@ WsLayout ws_layout(const am_model* m, int64_t B, int64_t N) {
   w.dc = take(B * H * 4);
   w.c0 = take(L * B * H * 4);
   w.h0 = take(L * B * H * e);
-  const int64_t cols = G > m->classes ? G : m->classes;
-  w.colsum = take(WsLayout::COLSUM_CHUNKS * cols * 4);
+  // split-K partials of the weight-gradient products (plus partial row sums)
+  const int64_t D0 = m->input_dim;
+  const int64_t wide = (D0 > H ? D0 : H) + H;
+  int64_t mn = G * wide + G;
+  if ((int64_t)m->classes * H + m->classes > mn) mn = (int64_t)m->classes * H + m->classes;
+  w.splitk_floats = WsLayout::MAX_SPLITS * mn;
+  w.splitk = take(w.splitk_floats * 4);
+  // step-barrier counters of the persistent kernels (one per 64 sequences)
+  // and their error flag
+  w.sync = take(((B + 63) / 64 + 64) * 4);
   w.total = pos;
   return w;
 }
@@ -218,6 +247,26 @@ am::GemmArgs mk_gemm(const void* A, int64_t lda, bool ak, const void* B, int64_t
   g.B = B; g.ldb = ldb; g.b_kmajor = bk;
   g.C = C; g.ldc = ldc; g.c_f32 = cf32;
   g.bias = bias; g.M = M; g.N = N; g.K = K; g.bf16 = bf16;
+  return g;
+}
+
+// Weight gradient  [C | C2] = A^T [B | B2]  (K = frames), fp32, with the
+// row sums of A (the bias gradient) and split-K scratch from the workspace.
+am::GemmArgs mk_wgrad(const void* A, int64_t lda, const void* B, int64_t ldb, int nB,
+                      const void* B2, int64_t ldb2, int nB2, float* C, int64_t ldc, float* C2,
+                      int64_t ldc2, float* rowsum, int M, int K, bool bf16, float* ws,
+                      int64_t ws_floats) {
+  am::GemmArgs g;
+  g.A = A; g.lda = lda; g.a_kmajor = false;
+  g.B = B; g.ldb = ldb; g.b_kmajor = false;
+  g.C = C; g.ldc = ldc; g.c_f32 = true;
+  if (B2) {
+    g.B2 = B2; g.ldb2 = ldb2; g.n_split = nB;
+    g.C2 = C2; g.ldc2 = ldc2;
+  }
+  g.rowsum = rowsum;
+  g.M = M; g.N = nB + (B2 ? nB2 : 0); g.K = K; g.bf16 = bf16;
+  g.ws = ws; g.ws_floats = ws_floats;
   return g;
 }
 
@@ -393,6 +442,28 @@ am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
                             (int)sc.N, (int)G, (int)D, bf), s));
     const char* Hl = at<char>(ws, w.h[l]);
     const float* Cl = at<float>(ws, w.c[l]);
+    if (sc.N > 0 && persistent_enabled() &&
+        am::lstm_persistent_fits(true, (int)H, B, bf, T)) {
+      am::PersistFwd pa;
+      pa.P = at<void>(ws, w.p_da);
+      pa.Wh = P8 + po.wh[l] * e;
+      pa.h0 = h0 ? at<char>(ws, w.h0) + (int64_t)l * B * H * e : nullptr;
+      pa.c0 = at<float>(ws, w.c0) + (int64_t)l * B * H;
+      pa.H = at<void>(ws, w.h[l]);
+      pa.Hs = at<void>(ws, w.hs[l]);
+      pa.C = at<float>(ws, w.c[l]);
+      pa.G = at<void>(ws, w.g[l]);
+      pa.counters = at<unsigned>(ws, w.sync);
+      pa.err = at<int>(ws, w.sync) + (B + 63) / 64;
+      pa.hidden = (int)H;
+      AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), (B + 63) / 64 + 1, s), "counters"));
+      const double bytes = (double)sc.N * (G * e * 2 + H * (2 * e + 4)) + (double)G * H * e;
+      Timed tm(AM_K_LSTM_FWD, s, 2.0 * sc.N * G * H, bytes);
+      bool used = false;
+      AM_TRY(hip_check(am::lstm_fwd_persistent(pa, persist_schedule(sc), bf, s, &used),
+                       "lstm forward layer"));
+      if (used) continue;
+    }
     for (int t = 0; t < T; ++t) {
       const int64_t nb = sc.counts[t];
       if (nb == 0) break;
@@ -471,17 +542,14 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
   const int N = (int)sc.N;
   const Offsets po = param_layout(m);
   const char* P8 = static_cast<const char*>(params);
-  float* colws = at<float>(ws, w.colsum);
+  float* skws = at<float>(ws, w.splitk);
 
-  // output layer: dWo = dZ^T H_top, dbo = column sums of dZ, dH_top = dZ Wo
+  // output layer: dWo = dZ^T H_top and dbo = column sums of dZ (one pass),
+  // then dH_top = dZ Wo
   AM_TRY(run_gemm(AM_K_GEMM_BWD_WGT,
-                  mk_gemm(dlogits, Cc, false, at<void>(ws, w.h[L - 1]), H, false, grads + po.wo, H,
-                          true, nullptr, (int)Cc, (int)H, N, bf), s));
-  {
-    Timed tm(AM_K_MISC, s, (double)N * Cc, (double)N * Cc * e);
-    AM_TRY(hip_check(am::colsum(dlogits, N, (int)Cc, bf, grads + po.bo, colws,
-                                WsLayout::COLSUM_CHUNKS, s), "bias gradient"));
-  }
+                  mk_wgrad(dlogits, Cc, at<void>(ws, w.h[L - 1]), H, (int)H, nullptr, 0, 0,
+                           grads + po.wo, H, nullptr, 0, grads + po.bo, (int)Cc, N, bf, skws,
+                           w.splitk_floats), s));
   void* DH = at<void>(ws, w.dh);
   AM_TRY(run_gemm(AM_K_GEMM_BWD_DATA,
                   mk_gemm(dlogits, Cc, true, P8 + po.wo * e, H, false, DH, H, false, nullptr, N,
@@ -492,13 +560,32 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
   float* dc = at<float>(ws, w.dc);
   for (int l = L - 1; l >= 0; --l) {
     const int64_t D = l == 0 ? m->input_dim : H;
-    {
+    const char* Gl = at<char>(ws, w.g[l]);
+    const float* Cl = at<float>(ws, w.c[l]);
+    bool used = false;
+    if (sc.N > 0 && persistent_enabled() &&
+        am::lstm_persistent_fits(false, (int)H, B, bf, T)) {
+      am::PersistBwd pa;
+      pa.Wh = P8 + po.wh[l] * e;
+      pa.dHa = DH;
+      pa.G = Gl;
+      pa.C = Cl;
+      pa.c0 = at<float>(ws, w.c0) + (int64_t)l * B * H;
+      pa.dA = dA;
+      pa.counters = at<unsigned>(ws, w.sync);
+      pa.err = at<int>(ws, w.sync) + (B + 63) / 64;
+      pa.hidden = (int)H;
+      AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), (B + 63) / 64 + 1, s), "counters"));
+      const double bytes = (double)sc.N * (G * e * 2 + H * (e + 8)) + (double)G * H * e;
+      Timed tm(AM_K_LSTM_BWD, s, 2.0 * (sc.N - sc.counts[0]) * G * H, bytes);
+      AM_TRY(hip_check(am::lstm_bwd_persistent(pa, persist_schedule(sc), bf, s, &used),
+                       "lstm backward layer"));
+    }
+    if (!used) {
       Timed tm(AM_K_MISC, s, 0.0, 2.0 * G * H * e);
       AM_TRY(hip_check(am::transpose(P8 + po.wh[l] * e, WhT, (int)G, (int)H, bf, s), "Wh transpose"));
     }
-    const char* Gl = at<char>(ws, w.g[l]);
-    const float* Cl = at<float>(ws, w.c[l]);
-    for (int t = T - 1; t >= 0; --t) {
+    for (int t = T - 1; t >= 0 && !used; --t) {
       const int64_t nb = sc.counts[t];
       if (nb == 0) continue;
       const int64_t nbn = t + 1 < T ? sc.counts[t + 1] : 0;
@@ -522,17 +609,11 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
       AM_TRY(hip_check(am::lstm_bwd_step(a, s), "lstm backward step"));
     }
     const void* X = l == 0 ? x : at<void>(ws, w.h[l - 1]);
+    // [dWx | dWh] = dA^T [X | Hs] and db = column sums of dA, one pass
     AM_TRY(run_gemm(AM_K_GEMM_BWD_WGT,
-                    mk_gemm(dA, G, false, X, D, false, grads + po.wx[l], D, true, nullptr, (int)G,
-                            (int)D, N, bf), s));
-    AM_TRY(run_gemm(AM_K_GEMM_BWD_WGT,
-                    mk_gemm(dA, G, false, at<void>(ws, w.hs[l]), H, false, grads + po.wh[l], H,
-                            true, nullptr, (int)G, (int)H, N, bf), s));
-    {
-      Timed tm(AM_K_MISC, s, (double)N * G, (double)N * G * e);
-      AM_TRY(hip_check(am::colsum(dA, N, (int)G, bf, grads + po.b[l], colws,
-                                  WsLayout::COLSUM_CHUNKS, s), "bias gradient"));
-    }
+                    mk_wgrad(dA, G, X, D, (int)D, at<void>(ws, w.hs[l]), H, (int)H,
+                             grads + po.wx[l], D, grads + po.wh[l], H, grads + po.b[l], (int)G, N,
+                             bf, skws, w.splitk_floats), s));
     if (l > 0)
       AM_TRY(run_gemm(AM_K_GEMM_BWD_DATA,
                       mk_gemm(dA, G, true, P8 + po.wx[l] * e, D, false, DH, H, false, nullptr, N,

@@ -48,20 +48,45 @@ __global__ __launch_bounds__(256) void lstm_fwd_step_kernel(
 #pragma unroll
     for (int g = 0; g < 4; ++g) acc[i][g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // operands of the cell update (independent of the product); rows past the
+  // active ones read a valid row (clamped) and are never stored
+  const int j = j0 + mfma_col(lane);
+  const int G4 = 4 * H;
+  T pin[4][4], hp[4];
+  float cpv[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int row = min(b0 + wave * 16 + mfma_row(lane, r), nb - 1);
+    const T* prow = P + (int64_t)row * G4;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) pin[r][g] = prow[g * H + j];
+    cpv[r] = cprev ? cprev[(int64_t)row * H + j] : 0.f;
+    hp[r] = hprev ? hprev[(int64_t)row * H + j] : from_f32<T>(0.f);
+  }
+
   if (hprev) {
     for (int ks = wave; ks < ksteps; ks += 4) {
       const int k = ks * 32 + koct;
       const bool kin = k < H;
+      const int kc = kin ? k : 0;
+      // Clamped, unmasked A loads: an output row depends only on its own A
+      // row and rows past the active ones are not stored.  Only a ragged
+      // k-tail (H % 32 != 0) zeroes the B fragments past H.
       Frag<T> a[4], b[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = b0 + i * 16 + (lane & 15);
-        a[i] = (kin && row < nb) ? frag_load<T>(hprev + (int64_t)row * H + k) : frag_zero<T>();
+        const int row = min(b0 + i * 16 + (lane & 15), nb - 1);
+        a[i] = frag_load<T>(hprev + (int64_t)row * H + kc);
       }
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int wrow = g * H + j0 + (lane & 15);
-        b[g] = kin ? frag_load<T>(Wh + (int64_t)wrow * H + k) : frag_zero<T>();
+        b[g] = frag_load<T>(Wh + (int64_t)wrow * H + kc);
+      }
+      if (H % 32 != 0) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          if (!kin) b[g] = frag_zero<T>();
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -85,25 +110,21 @@ __global__ __launch_bounds__(256) void lstm_fwd_step_kernel(
     s[g] += red[3][wave][g][lane];
   }
 
-  const int j = j0 + mfma_col(lane);
-  const int G4 = 4 * H;
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int row = b0 + wave * 16 + mfma_row(lane, r);
     if (row >= nb) continue;
-    const T* prow = P + (int64_t)row * G4;
-    const float ai = s[0][r] + to_f32<T>(prow[j]);
-    const float af = s[1][r] + to_f32<T>(prow[H + j]);
-    const float ag = s[2][r] + to_f32<T>(prow[2 * H + j]);
-    const float ao = s[3][r] + to_f32<T>(prow[3 * H + j]);
+    const float ai = s[0][r] + to_f32<T>(pin[r][0]);
+    const float af = s[1][r] + to_f32<T>(pin[r][1]);
+    const float ag = s[2][r] + to_f32<T>(pin[r][2]);
+    const float ao = s[3][r] + to_f32<T>(pin[r][3]);
     const float gi = sigm(ai), gf = sigm(af), gg = tanh_f(ag), go = sigm(ao);
-    const float cp = cprev ? cprev[(int64_t)row * H + j] : 0.f;
-    const float c = gf * cp + gi * gg;
+    const float c = gf * cpv[r] + gi * gg;
     const float h = go * tanh_f(c);
     const int64_t o = (int64_t)row * H + j;
     Cout[o] = c;
     Hout[o] = from_f32<T>(h);
-    Hs[o] = hprev ? hprev[o] : from_f32<T>(0.f);
+    Hs[o] = hp[r];
     T* grow = G + (int64_t)row * G4;
     grow[j] = from_f32<T>(gi);
     grow[H + j] = from_f32<T>(gf);
@@ -130,14 +151,35 @@ __global__ __launch_bounds__(256) void lstm_bwd_step_kernel(
 #pragma unroll
   for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // operands of the cell backward (independent of the product); rows past
+  // the active ones read a valid row (clamped) and are never stored
+  const int j = j0 + mfma_col(lane);
+  T gv[4][4], dhv[4];
+  float cv[4], cpv[4], dcv[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int row0 = b0 + wave * 16 + mfma_row(lane, r);
+    const int row = min(row0, nb - 1);
+    const int64_t o = (int64_t)row * H + j;
+    const T* grow = G + (int64_t)row * G4;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) gv[r][g] = grow[g * H + j];
+    cv[r] = C[o];
+    cpv[r] = Cprev ? Cprev[o] : 0.f;
+    dcv[r] = dc[o];  // used only where the sequence continues to t+1
+    dhv[r] = dHa[o];
+    (void)row0;
+  }
+
   if (dAnext && b0 < nbn) {
     for (int ks = wave; ks < ksteps; ks += 4) {
       const int k = ks * 32 + koct;
+      // clamped, unmasked loads; rows without a step t+1 are zeroed below
       Frag<T> a[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = b0 + i * 16 + (lane & 15);
-        a[i] = row < nbn ? frag_load<T>(dAnext + (int64_t)row * G4 + k) : frag_zero<T>();
+        const int row = min(b0 + i * 16 + (lane & 15), nbn - 1);
+        a[i] = frag_load<T>(dAnext + (int64_t)row * G4 + k);
       }
       const Frag<T> b = frag_load<T>(WhT + (int64_t)(j0 + (lane & 15)) * G4 + k);
 #pragma unroll
@@ -153,23 +195,19 @@ __global__ __launch_bounds__(256) void lstm_bwd_step_kernel(
   s += red[2][wave][lane];
   s += red[3][wave][lane];
 
-  const int j = j0 + mfma_col(lane);
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int row = b0 + wave * 16 + mfma_row(lane, r);
     if (row >= nb) continue;
     const int64_t o = (int64_t)row * H + j;
-    const T* grow = G + (int64_t)row * G4;
-    const float gi = to_f32<T>(grow[j]), gf = to_f32<T>(grow[H + j]);
-    const float gg = to_f32<T>(grow[2 * H + j]), go = to_f32<T>(grow[3 * H + j]);
-    const float c = C[o];
-    const float cp = Cprev ? Cprev[o] : 0.f;
-    const float dcn = row < nbn ? dc[o] : 0.f;
-    const float dh = to_f32<T>(dHa[o]) + s[r];
-    const float tc = tanh_f(c);
+    const float gi = to_f32<T>(gv[r][0]), gf = to_f32<T>(gv[r][1]);
+    const float gg = to_f32<T>(gv[r][2]), go = to_f32<T>(gv[r][3]);
+    const bool cont = row < nbn;  // the sequence continues to step t+1
+    const float dh = to_f32<T>(dhv[r]) + (cont ? s[r] : 0.f);
+    const float tc = tanh_f(cv[r]);
     const float d_o = dh * tc;
-    const float dcell = dh * go * (1.f - tc * tc) + dcn;
-    const float d_i = dcell * gg, d_g = dcell * gi, d_f = dcell * cp;
+    const float dcell = dh * go * (1.f - tc * tc) + (cont ? dcv[r] : 0.f);
+    const float d_i = dcell * gg, d_g = dcell * gi, d_f = dcell * cpv[r];
     dc[o] = dcell * gf;
     T* arow = dA + (int64_t)row * G4;
     arow[j] = from_f32<T>(d_i * gi * (1.f - gi));

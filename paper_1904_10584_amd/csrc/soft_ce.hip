@@ -51,6 +51,18 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
         if (c < C) store4<DT>(dr + c, make_float4(0.f, 0.f, 0.f, 0.f));
       }
     } else {
+      // teacher entries: lane j holds entry j (K <= 64 per pass); their
+      // loads overlap the row loads below
+      const int32_t* ir = idx + f * K;
+      const float* pr = prob + f * K;
+      int tc = -1;
+      float tp = 0.f, tz = 0.f;
+      if (lane < K) {
+        tc = ir[lane];
+        tp = pr[lane];
+        if (tc < 0 || tc >= C) { tc = -1; tp = 0.f; }  // empty slot (or out of range)
+        else tz = zr[tc];
+      }
       float4 v[NCH];
       float mx = -INFINITY;
 #pragma unroll
@@ -71,16 +83,19 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
       se = wave_sum(se);
       const float lse = mx + __logf(se);
 
-      const int32_t* ir = idx + f * K;
-      const float* pr = prob + f * K;
-      float mass = 0.f, lf = 0.f;
-      for (int jj = 0; jj < K; ++jj) {
-        const int c = ir[jj];
-        if (c < 0 || c >= C) continue;  // empty slot (or out of range: ignored)
-        const float p = pr[jj];
-        mass += p;
-        lf -= p * (zr[c] - lse);
+      float mass = tp, lf = tc >= 0 ? -tp * (tz - lse) : 0.f;
+      for (int j0 = 64; j0 < K; j0 += 64) {  // more than 64 entries per frame
+        const int j = j0 + lane;
+        if (j < K) {
+          const int c = ir[j];
+          if (c >= 0 && c < C) {
+            mass += pr[j];
+            lf -= pr[j] * (zr[c] - lse);
+          }
+        }
       }
+      mass = wave_sum(mass);
+      lf = wave_sum(lf);
       const float sm = s * mass;
 #pragma unroll
       for (int i = 0; i < NCH; ++i) {
@@ -90,10 +105,19 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
         v[i].w = sm * __expf(v[i].w - lse);
       }
       for (int jj = 0; jj < K; ++jj) {
-        const int c = ir[jj];
-        if (c < 0 || c >= C) continue;
+        int c;
+        float p;
+        if (jj < 64) {  // broadcast entry jj from the lane that loaded it
+          c = __builtin_amdgcn_readlane(tc, jj);
+          p = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, tp), jj));
+        } else {
+          c = ir[jj];
+          p = pr[jj];
+          if (c >= C) c = -1;
+        }
+        if (c < 0) continue;
         const int ci = c >> 8, owner = (c & 255) >> 2, cc = c & 3;
-        const float d = lane == owner ? s * pr[jj] : 0.f;
+        const float d = lane == owner ? s * p : 0.f;
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
           if (i == ci) {  // wave-uniform

@@ -145,6 +145,7 @@ def _ce_case(N, C, K, seed, empty_slots=False, dup=False, mask=False):
 @pytest.mark.parametrize("N,C,K,opts", [
     (1, 4, 1, {}), (37, 500, 5, {"empty_slots": True}), (1000, 3000, 20, {"dup": True}),
     (130, 8192, 20, {"mask": True}), (257, 6000, 1, {}), (64, 260, 3, {"mask": True, "empty_slots": True}),
+    (50, 512, 100, {"empty_slots": True, "dup": True}),
 ])
 @pytest.mark.parametrize("dz_bf16", [False, True])
 @pytest.mark.parametrize("reduction", [am.MEAN_VALID, am.SUM])

@@ -18,6 +18,17 @@ F32_TOL = 1e-4
 BF16_TOL = 2e-2
 
 
+@pytest.fixture(params=["persistent", "single_step"], autouse=True)
+def recurrence_path(request, monkeypatch):
+    """Every test runs with the persistent layer kernels and again with one
+    launch per time step."""
+    if request.param == "single_step":
+        monkeypatch.setenv("AM_STEP_KERNELS", "1")
+    else:
+        monkeypatch.delenv("AM_STEP_KERNELS", raising=False)
+    return request.param
+
+
 def _problem(dims, T, B, K, mass, lengths=None, seed=0, state=False, one_hot_frac=0.0):
     counts, offs = oracle.batch_schedule(T, B, lengths)
     N = int(offs[-1])
