@@ -180,6 +180,7 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     am.profile_end()
+    st.check()  # a timed-out step barrier invalidates the measurement
     kt = am.profile_get(dom)
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     flops, N = step_flops(w, T, lengths)

@@ -53,7 +53,8 @@ typedef enum {
   AM_ECAPACITY = -2,     /* an output buffer is too small */
   AM_EUNSUPPORTED = -3,  /* valid but outside what the kernels handle */
   AM_EHIP = -4,          /* a HIP call failed (launch error, ...) */
-  AM_EWORKSPACE = -5     /* workspace missing or too small */
+  AM_EWORKSPACE = -5,    /* workspace missing or too small */
+  AM_ETIMEOUT = -6       /* a step barrier timed out; the pass's results are invalid */
 } am_status;
 
 typedef enum { AM_F32 = 0, AM_BF16 = 1 } am_dtype;
@@ -132,6 +133,15 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
                            const void* dlogits, void* ws, int64_t ws_bytes,
                            float* grads, void* stream);
 
+/* Whether the recurrence of the last lstm_am_forward (and lstm_am_backward)
+ * on `ws` completed.  The recurrence runs as one persistent launch per layer
+ * whose workgroups meet at a barrier every time step; each wait is bounded,
+ * and a wait that runs out (workgroups not co-resident, a stalled device)
+ * sets a flag in `ws` instead of hanging.  Synchronises `stream`, then
+ * returns AM_OK, or AM_ETIMEOUT when the flag is set (the outputs of that
+ * pass must be discarded).  The flag is cleared by the next forward call. */
+am_status am_workspace_check(const void* ws, int64_t ws_bytes, void* stream);
+
 /* Gradient Threshold Compression encode (§VI-A), exact fp32:
  *   for i in 0..n-1:  a = residual[i] + grad[i]
  *     a >  tau: residual[i] = a - tau, emit (i << 1) | 0
@@ -170,8 +180,8 @@ typedef enum {
   AM_K_GEMM_FWD = 0,      /* input and output projections */
   AM_K_GEMM_BWD_DATA = 1, /* gradients into activations (dlogits Wo, dA Wx) */
   AM_K_GEMM_BWD_WGT = 2,  /* weight gradients (reductions over frames) */
-  AM_K_LSTM_FWD = 3,      /* recurrent product + cell, one step */
-  AM_K_LSTM_BWD = 4,      /* recurrent product + cell backward, one step */
+  AM_K_LSTM_FWD = 3,      /* recurrent product + cell (a layer's launch, or a step's) */
+  AM_K_LSTM_BWD = 4,      /* recurrent product + cell backward (likewise) */
   AM_K_CE = 5,            /* soft-target cross-entropy rows */
   AM_K_ENCODE = 6,        /* threshold encode (all of its kernels) */
   AM_K_DECODE = 7,

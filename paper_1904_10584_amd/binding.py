@@ -20,7 +20,7 @@ F32, BF16 = 0, 1
 MEAN_VALID, SUM = 0, 1
 K_GEMM_FWD, K_GEMM_BWD_DATA, K_GEMM_BWD_WGT, K_LSTM_FWD, K_LSTM_BWD = 0, 1, 2, 3, 4
 K_CE, K_ENCODE, K_DECODE, K_SGD, K_MISC = 5, 6, 7, 8, 9
-KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd_data", "gemm_bwd_wgt", "lstm_fwd_step", "lstm_bwd_step",
+KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd_data", "gemm_bwd_wgt", "lstm_fwd", "lstm_bwd",
                   "soft_ce", "encode", "decode", "sgd", "misc"]
 
 
@@ -67,6 +67,7 @@ _PROTOS = {
     "grad_threshold_decode": (_I32, [_P, _P, _I64, _F32, _I64, _P, _I32, _P]),
     "sgd_apply": (_I32, [_I64, _P, _P, _P, _F32, _P]),
     "am_cast_f32_to_bf16": (_I32, [_I64, _P, _P, _P]),
+    "am_workspace_check": (_I32, [_P, _I64, _P]),
     "am_profile_begin": (_I32, [ctypes.c_uint32]),
     "am_profile_end": (_I32, []),
     "am_profile_get": (_I32, [_I32, _P, _P, _P, _P]),
@@ -189,6 +190,13 @@ def sparse_soft_ce(logits, idx, prob, loss, dlogits, ws, mask=None, reduction=ME
         _dev(prob, "prob", torch.float32), _dev(mask, "mask", torch.uint8), reduction,
         _dev(loss, "loss", torch.float32), _dev(dlogits, "dlogits"), dt, _dev(ws, "ws"),
         ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def workspace_check(ws, stream=None):
+    """Synchronise the stream; raise AmError if a step barrier of the last
+    forward/backward pass on `ws` timed out (its outputs are then invalid)."""
+    _check(lib().am_workspace_check(_dev(ws, "ws"), ws.numel() * ws.element_size(),
+                                    _stream(stream)))
 
 
 def grad_threshold_encode(grad, residual, tau, words, count, ws, stream=None):

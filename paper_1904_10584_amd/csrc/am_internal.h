@@ -94,6 +94,22 @@ struct PersistBwd {
   int* err;
   int hidden;
 };
+// XCD-local persistent layer kernels (one block of sequences per XCD, the
+// exchange and the step barrier inside that XCD's L2).  Scratch: one step
+// counter per block at flags[32 blk] (one cache line each), a start counter
+// and the XCC id of every workgroup (xcc[grid]), all zero at launch, and the
+// time-out flag (set, never cleared).
+struct XcdSync {
+  unsigned* flags;
+  unsigned* start;
+  int* xcc;
+  int* err;
+  int units;  // filled in by the launcher
+};
+bool lstm_xcd_instantiated(bool forward, int hidden, int B);
+hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used);
+hipError_t lstm_bwd_xcd_launch(PersistBwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used);
+
 // Whether the persistent kernel covers this shape and its grid can be
 // resident at once on the current device.
 bool lstm_persistent_fits(bool forward, int hidden, int B, bool bf16, int T);

@@ -82,6 +82,7 @@ class Timed {
   ~Timed() {
     if (active_ && hipEventRecord(rec_.b, s_) == hipSuccess) g_prof.recs.push_back(rec_);
   }
+  void cancel() { active_ = false; }  // nothing was launched
 
  private:
   hipStream_t s_;
@@ -168,7 +169,40 @@ am_status make_schedule(int32_t T, int32_t B, const int32_t* lengths, Schedule& 
 // the environment forces one launch per time step instead.
 bool persistent_enabled() {
   const char* v = getenv("AM_STEP_KERNELS");
-  return !(v && v[0] && v[0] != '0');
+  if (v && v[0] && v[0] != '0') return false;
+  const char* r = getenv("AM_RECURRENCE");
+  return !(r && strcmp(r, "step") == 0);
+}
+
+// AM_RECURRENCE=xcd|device|step picks one recurrence path (for tests);
+// unset, the XCD-local kernels are tried first, then the device-scope ones.
+bool xcd_enabled() {
+  const char* r = getenv("AM_RECURRENCE");
+  return persistent_enabled() && !(r && strcmp(r, "device") == 0);
+}
+bool device_persistent_enabled() {
+  const char* r = getenv("AM_RECURRENCE");
+  return persistent_enabled() && !(r && strcmp(r, "xcd") == 0);
+}
+
+// Scratch of the persistent kernels: the sync region at offset 0 of the
+// workspace.  Its first SYNC_CLEAR_WORDS words (step counters, start counter,
+// XCC ids) are zeroed before every launch; its last word is the barrier
+// time-out flag, zeroed once per forward pass and only ever set afterwards,
+// so a time-out anywhere in a forward + backward pair stays visible to
+// am_workspace_check.
+constexpr int64_t SYNC_BYTES = 8192;
+constexpr int64_t SYNC_CLEAR_WORDS = SYNC_BYTES / 4 - 64;
+constexpr int64_t SYNC_STICKY_WORD = SYNC_BYTES / 4 - 1;
+am::XcdSync xcd_sync(void* base) {
+  unsigned* u = static_cast<unsigned*>(base);
+  am::XcdSync y;
+  y.flags = u;             // counter of block k at u[32 k]
+  y.start = u + 256;
+  y.err = reinterpret_cast<int*>(u + SYNC_STICKY_WORD);
+  y.xcc = reinterpret_cast<int*>(u + 260);  // up to 1024 workgroups
+  y.units = 0;
+  return y;
 }
 
 am::PersistSchedule persist_schedule(const Schedule& sc) {
@@ -199,6 +233,8 @@ WsLayout ws_layout(const am_model* m, int64_t B, int64_t N) {
   const int64_t e = esz_of(m->dtype), H = m->hidden, G = 4 * H, L = m->layers;
   int64_t pos = 0;
   auto take = [&](int64_t bytes) { int64_t at = pos; pos += align256(bytes); return at; };
+  // step-barrier scratch of the persistent kernels and the time-out flag
+  w.sync = take(SYNC_BYTES);
   for (int l = 0; l < L; ++l) {
     w.h.push_back(take(N * H * e));
     w.hs.push_back(take(N * H * e));
@@ -218,9 +254,6 @@ WsLayout ws_layout(const am_model* m, int64_t B, int64_t N) {
   if ((int64_t)m->classes * H + m->classes > mn) mn = (int64_t)m->classes * H + m->classes;
   w.splitk_floats = WsLayout::MAX_SPLITS * mn;
   w.splitk = take(w.splitk_floats * 4);
-  // step-barrier counters of the persistent kernels (one per 64 sequences)
-  // and their error flag
-  w.sync = take(((B + 63) / 64 + 64) * 4);
   w.total = pos;
   return w;
 }
@@ -284,6 +317,7 @@ const char* am_status_string(int32_t st) {
     case AM_EUNSUPPORTED: return "unsupported configuration";
     case AM_EHIP: return "HIP error";
     case AM_EWORKSPACE: return "workspace missing or too small";
+    case AM_ETIMEOUT: return "step barrier timed out";
     default: return "unknown status";
   }
 }
@@ -431,6 +465,8 @@ am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
     if (c0) AM_TRY(hip_check(am::convert_rows(c0, c0w, L * B * H, false, s), "c0 copy"));
     else AM_TRY(hip_check(am::fill_zero(c0w, L * B * H, s), "c0 clear"));
     if (h0) AM_TRY(hip_check(am::convert_rows(h0, at<void>(ws, w.h0), L * B * H, bf, s), "h0 convert"));
+    // a new forward + backward pair: clear the barrier time-out flag too
+    AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_BYTES / 4, s), "sync clear"));
   }
 
   for (int l = 0; l < L; ++l) {
@@ -442,8 +478,7 @@ am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
                             (int)sc.N, (int)G, (int)D, bf), s));
     const char* Hl = at<char>(ws, w.h[l]);
     const float* Cl = at<float>(ws, w.c[l]);
-    if (sc.N > 0 && persistent_enabled() &&
-        am::lstm_persistent_fits(true, (int)H, B, bf, T)) {
+    if (sc.N > 0 && persistent_enabled()) {
       am::PersistFwd pa;
       pa.P = at<void>(ws, w.p_da);
       pa.Wh = P8 + po.wh[l] * e;
@@ -454,14 +489,25 @@ am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
       pa.C = at<float>(ws, w.c[l]);
       pa.G = at<void>(ws, w.g[l]);
       pa.counters = at<unsigned>(ws, w.sync);
-      pa.err = at<int>(ws, w.sync) + (B + 63) / 64;
+      pa.err = at<int>(ws, w.sync) + SYNC_STICKY_WORD;
       pa.hidden = (int)H;
-      AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), (B + 63) / 64 + 1, s), "counters"));
+      const am::PersistSchedule ps = persist_schedule(sc);
+      const double flops = 2.0 * sc.N * G * H;
       const double bytes = (double)sc.N * (G * e * 2 + H * (2 * e + 4)) + (double)G * H * e;
-      Timed tm(AM_K_LSTM_FWD, s, 2.0 * sc.N * G * H, bytes);
       bool used = false;
-      AM_TRY(hip_check(am::lstm_fwd_persistent(pa, persist_schedule(sc), bf, s, &used),
-                       "lstm forward layer"));
+      if (bf && xcd_enabled() && am::lstm_xcd_instantiated(true, (int)H, B)) {
+        AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
+        Timed tm(AM_K_LSTM_FWD, s, flops, bytes);
+        AM_TRY(hip_check(am::lstm_fwd_xcd_launch(pa, ps, xcd_sync(at<void>(ws, w.sync)), s, &used),
+                         "lstm forward layer (xcd)"));
+        if (!used) tm.cancel();
+      }
+      if (!used && device_persistent_enabled() && am::lstm_persistent_fits(true, (int)H, B, bf, T)) {
+        AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
+        Timed tm(AM_K_LSTM_FWD, s, flops, bytes);
+        AM_TRY(hip_check(am::lstm_fwd_persistent(pa, ps, bf, s, &used), "lstm forward layer"));
+        if (!used) tm.cancel();
+      }
       if (used) continue;
     }
     for (int t = 0; t < T; ++t) {
@@ -563,8 +609,7 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
     const char* Gl = at<char>(ws, w.g[l]);
     const float* Cl = at<float>(ws, w.c[l]);
     bool used = false;
-    if (sc.N > 0 && persistent_enabled() &&
-        am::lstm_persistent_fits(false, (int)H, B, bf, T)) {
+    if (sc.N > 0 && persistent_enabled()) {
       am::PersistBwd pa;
       pa.Wh = P8 + po.wh[l] * e;
       pa.dHa = DH;
@@ -573,13 +618,24 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
       pa.c0 = at<float>(ws, w.c0) + (int64_t)l * B * H;
       pa.dA = dA;
       pa.counters = at<unsigned>(ws, w.sync);
-      pa.err = at<int>(ws, w.sync) + (B + 63) / 64;
+      pa.err = at<int>(ws, w.sync) + SYNC_STICKY_WORD;
       pa.hidden = (int)H;
-      AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), (B + 63) / 64 + 1, s), "counters"));
+      const am::PersistSchedule ps = persist_schedule(sc);
+      const double flops = 2.0 * (sc.N - sc.counts[0]) * G * H;
       const double bytes = (double)sc.N * (G * e * 2 + H * (e + 8)) + (double)G * H * e;
-      Timed tm(AM_K_LSTM_BWD, s, 2.0 * (sc.N - sc.counts[0]) * G * H, bytes);
-      AM_TRY(hip_check(am::lstm_bwd_persistent(pa, persist_schedule(sc), bf, s, &used),
-                       "lstm backward layer"));
+      if (bf && xcd_enabled() && am::lstm_xcd_instantiated(false, (int)H, B)) {
+        AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
+        Timed tm(AM_K_LSTM_BWD, s, flops, bytes);
+        AM_TRY(hip_check(am::lstm_bwd_xcd_launch(pa, ps, xcd_sync(at<void>(ws, w.sync)), s, &used),
+                         "lstm backward layer (xcd)"));
+        if (!used) tm.cancel();
+      }
+      if (!used && device_persistent_enabled() && am::lstm_persistent_fits(false, (int)H, B, bf, T)) {
+        AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
+        Timed tm(AM_K_LSTM_BWD, s, flops, bytes);
+        AM_TRY(hip_check(am::lstm_bwd_persistent(pa, ps, bf, s, &used), "lstm backward layer"));
+        if (!used) tm.cancel();
+      }
     }
     if (!used) {
       Timed tm(AM_K_MISC, s, 0.0, 2.0 * G * H * e);
@@ -623,6 +679,18 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
 }
 
 // ---------------------------------------------------------------- timing --
+
+am_status am_workspace_check(const void* ws, int64_t ws_bytes, void* stream) {
+  if (!ws || !aligned(ws, 256)) return fail(AM_EINVAL, "NULL or unaligned workspace");
+  if (ws_bytes < SYNC_BYTES) return fail(AM_EWORKSPACE, "workspace smaller than its sync region");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int flag = 0;
+  AM_TRY(hip_check(hipMemcpyAsync(&flag, static_cast<const char*>(ws) + SYNC_STICKY_WORD * 4,
+                                  sizeof flag, hipMemcpyDeviceToHost, s), "flag read"));
+  AM_TRY(hip_check(hipStreamSynchronize(s), "stream sync"));
+  if (flag) return fail(AM_ETIMEOUT, "a step barrier of a persistent recurrence kernel timed out");
+  return AM_OK;
+}
 
 am_status am_profile_begin(uint32_t class_mask) {
   g_prof.on = true;

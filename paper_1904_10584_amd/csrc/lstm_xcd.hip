@@ -1,0 +1,510 @@
+// XCD-local persistent LSTM layer kernels.
+//
+// The recurrence exchanges h_{t-1} (dA_{t+1} backward) between the
+// workgroups that share a block of sequences at every step.  MI355X has 8
+// XCDs, each with its own L2; an exchange through device memory pays a
+// write-back of the producer's L2, an invalidation of the consumer's, and
+// memory latency on every step.  Here the sequences are split into 8 blocks,
+// one per XCD, and the workgroups of a block all run on that XCD, so the
+// exchange and the step barrier stay inside one L2:
+//   * workgroup i serves block i % 8 and unit slice i / 8 (workgroups are
+//     dispatched to XCDs round-robin); at start every workgroup records its
+//     XCC id and, unless every block really is on one XCD, the kernel falls
+//     back to device-scope release/acquire for its whole run;
+//   * the step barrier is one counter per block, bumped with an atomic add
+//     by every member after its stores of the step have completed and
+//     polled by one lane with device-scope loads;
+//   * every exchanged row is written once and read only after it was written,
+//     so no consumer's L1 can hold a stale copy.
+// A workgroup owns U hidden units (U % 4 == 0) of one block of RB sequences
+// (RB = 16 or 32).  The forward product keeps the workgroup's 4U columns of
+// W_h resident in LDS in unit-major, gate-minor order, so a 16-column MFMA
+// tile holds 4 units x 4 gates; a per-wave transpose of 4x4 quads through
+// LDS then gives each lane all four gate pre-activations of one
+// (sequence, unit).  The backward product keeps the U rows of W_h^T in LDS.
+#include "am_device.h"
+#include "am_internal.h"
+
+namespace am {
+namespace {
+
+constexpr int NX = 8;                    // XCDs
+constexpr unsigned SPIN_LIMIT = 1u << 22;
+constexpr int FWD_LDS_W = 147456;        // bytes of resident weights, forward
+constexpr int BWD_LDS_W = 147456;        // bytes of resident weights, backward
+
+__device__ __forceinline__ unsigned xcc_id() {
+  unsigned v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return v & 0xfu;
+}
+
+// One-time check that every block's workgroups share one XCD.  Uses
+// device-scope atomics; returns the same answer in every workgroup.
+__device__ bool check_local(const XcdSync& y, int* bad_sh) {
+  const int n = gridDim.x;
+  if (threadIdx.x == 0) {
+    __hip_atomic_store(y.xcc + blockIdx.x, (int)xcc_id(), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_add(y.start, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    unsigned spins = 0;
+    while (__hip_atomic_load(y.start, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < (unsigned)n) {
+      if (++spins > SPIN_LIMIT) {
+        __hip_atomic_store(y.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    *bad_sh = 0;
+  }
+  __syncthreads();
+  int bad = 0;
+  for (int k = threadIdx.x; k < n; k += blockDim.x)
+    bad |= __hip_atomic_load(y.xcc + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) !=
+           __hip_atomic_load(y.xcc + (k % NX), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (bad) __hip_atomic_store(bad_sh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  __syncthreads();
+  return *bad_sh == 0;
+}
+
+// This workgroup's stores of the step have completed; count it in its
+// block's step counter.  Relaxed atomics are performed beyond the CU (in L2
+// or the memory side), so counter updates are seen by every poller; the
+// release fence (a write-back of this XCD's L2) is needed only when a block
+// spans XCDs.
+__device__ __forceinline__ void xsignal(const XcdSync& y, bool local) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned* cnt = y.flags + (blockIdx.x % NX) * 32;
+    if (!local) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Wait until the block's counter reaches `target` (members x steps).  One
+// lane polls with device-scope loads, which bypass the CU's L1; the other
+// workgroups' exchanged rows are then read from the shared L2 (local) or
+// after an acquire that invalidates this CU's caches (block spans XCDs).
+__device__ __forceinline__ void xwait(const XcdSync& y, bool local, unsigned target) {
+  if (threadIdx.x == 0) {
+    const unsigned* cnt = y.flags + (blockIdx.x % NX) * 32;
+    unsigned spins = 0;
+    while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      if (++spins > SPIN_LIMIT) {
+        __hip_atomic_store(y.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (!local) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ int active_down(const PersistSchedule& ps, int nb, int t) {
+  if (!ps.varlen) return ps.B;
+  while (nb > 0 && (int)ps.lens[nb - 1] <= t) --nb;
+  return nb;
+}
+__device__ __forceinline__ int active_up(const PersistSchedule& ps, int nb, int t) {
+  if (!ps.varlen) return ps.B;
+  while (nb < ps.B && (int)ps.lens[nb] > t) ++nb;
+  return nb;
+}
+
+// ----------------------------------------------------------------- forward --
+// MT: row tiles (RB = 16 MT); KS: k-steps (H = 32 KS); TPW: output tiles per wave.
+template <typename T, int MT, int KS, int TPW>
+__global__ __launch_bounds__(256, 1) void lstm_fwd_xcd(PersistFwd a, PersistSchedule ps, XcdSync y) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  Frag<T>* wl = reinterpret_cast<Frag<T>*>(lds);                       // [n][s][lane]
+  f32x4_t* xs = reinterpret_cast<f32x4_t*>(lds + FWD_LDS_W);            // [wave][tile][lane]
+  __shared__ int bad_sh;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int H = a.hidden, G4 = 4 * H, U = y.units;
+  const int NT = U / 4;                        // 16-column tiles = 4 units x 4 gates
+  const int ntiles = MT * NT;
+  const int blk = blockIdx.x % NX, us = blockIdx.x / NX;
+  const int b0 = blk * 16 * MT, j0 = us * U;
+  const int members = H / U;
+  const int koct = (lane >> 4) * 8;
+  const T* __restrict__ P = static_cast<const T*>(a.P);
+  const T* __restrict__ Wh = static_cast<const T*>(a.Wh);
+  const T* __restrict__ h0 = static_cast<const T*>(a.h0);
+  T* __restrict__ Hb = static_cast<T*>(a.H);
+  T* __restrict__ Hs = static_cast<T*>(a.Hs);
+  T* __restrict__ Gb = static_cast<T*>(a.G);
+
+  // resident weights: column c of tile n is unit j0 + 4n + c/4, gate c%4
+  for (int e = threadIdx.x; e < NT * KS * 64; e += 256) {
+    const int l = e & 63, s = (e >> 6) % KS, n = e / (64 * KS);
+    const int c = l & 15, k = s * 32 + (l >> 4) * 8;
+    const int row = (c & 3) * H + j0 + 4 * n + (c >> 2);
+    wl[e] = k < H ? frag_load<T>(Wh + (int64_t)row * H + k) : frag_zero<T>();
+  }
+  const bool local = check_local(y, &bad_sh);
+
+  // the lane's cells: tile t = wave + 4 ts -> row tile t % MT, column tile t / MT;
+  // row m*16 + 4(lane/16) + lane%4, unit j0 + 4n + (lane%16)/4
+  const int mw = wave % MT;
+  const int qrow = mw * 16 + 4 * (lane >> 4) + (lane & 3);
+  float c_reg[TPW];
+  T h_reg[TPW];
+#pragma unroll
+  for (int ts = 0; ts < TPW; ++ts) {
+    const int t = wave + 4 * ts;
+    const int j = j0 + 4 * (t / MT) + ((lane & 15) >> 2);
+    const int b = b0 + qrow;
+    const bool ok = t < ntiles && b < ps.B;
+    c_reg[ts] = ok ? a.c0[(int64_t)b * H + j] : 0.f;
+    h_reg[ts] = (ok && h0) ? h0[(int64_t)b * H + j] : from_f32<T>(0.f);
+  }
+
+  int nb = ps.B, off = 0, off_prev = 0;
+  for (int t = 0; t < ps.T; ++t) {
+    nb = active_down(ps, nb, t);
+    if (b0 >= nb) break;  // this block of sequences has ended for good
+
+    T pin[TPW][4];
+#pragma unroll
+    for (int ts = 0; ts < TPW; ++ts) {
+      const int tt = wave + 4 * ts;
+      const int j = j0 + 4 * ((tt < ntiles ? tt : 0) / MT) + ((lane & 15) >> 2);
+      const T* prow = P + (int64_t)(off + min(b0 + qrow, nb - 1)) * G4;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) pin[ts][g] = prow[g * H + j];
+    }
+
+    f32x4_t acc[TPW];
+#pragma unroll
+    for (int ts = 0; ts < TPW; ++ts) acc[ts] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    const T* hprev = h0;
+    if (t > 0) {
+      xwait(y, local, (unsigned)(members * t));
+      hprev = Hb + (int64_t)off_prev * H;
+    }
+    if (hprev) {
+      // all of the wave's A fragments in flight at once (clamped, unmasked)
+      const T* hrow = hprev + (int64_t)min(b0 + mw * 16 + (lane & 15), nb - 1) * H + koct;
+      Frag<T> af[KS];
+#pragma unroll
+      for (int s = 0; s < KS; ++s) af[s] = frag_load<T>(hrow + (s * 32 + koct < H ? s * 32 : 0));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int ts = 0; ts < TPW; ++ts) {
+        const int tt = wave + 4 * ts;
+        if (tt >= ntiles) break;
+        const Frag<T>* wn = wl + (tt / MT) * KS * 64 + lane;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) mma_16x16x32(acc[ts], af[s], wn[s * 64]);
+      }
+    }
+
+    // 4x4 quad transpose: lane l gets, for row 4(l/16) + l%4, the 4 gates
+    // of its unit from lanes (l & ~3) + g
+    f32x4_t* xw = xs + wave * TPW * 64;
+#pragma unroll
+    for (int ts = 0; ts < TPW; ++ts) xw[ts * 64 + lane] = acc[ts];
+    float gpre[TPW][4];
+#pragma unroll
+    for (int ts = 0; ts < TPW; ++ts)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        gpre[ts][g] = reinterpret_cast<const float*>(xw + ts * 64 + (lane & ~3) + g)[lane & 3];
+
+    const int b = b0 + qrow;
+#pragma unroll
+    for (int ts = 0; ts < TPW; ++ts) {
+      const int tt = wave + 4 * ts;
+      if (tt >= ntiles || b >= nb) continue;
+      const int j = j0 + 4 * (tt / MT) + ((lane & 15) >> 2);
+      const float gi = sigm(gpre[ts][0] + to_f32<T>(pin[ts][0]));
+      const float gf = sigm(gpre[ts][1] + to_f32<T>(pin[ts][1]));
+      const float gg = tanh_f(gpre[ts][2] + to_f32<T>(pin[ts][2]));
+      const float go = sigm(gpre[ts][3] + to_f32<T>(pin[ts][3]));
+      const float c = gf * c_reg[ts] + gi * gg;
+      const T h = from_f32<T>(go * tanh_f(c));
+      const int64_t o = (int64_t)(off + b) * H + j;
+      a.C[o] = c;
+      Hb[o] = h;
+      Hs[o] = h_reg[ts];
+      T* grow = Gb + (int64_t)(off + b) * G4;
+      grow[j] = from_f32<T>(gi);
+      grow[H + j] = from_f32<T>(gf);
+      grow[2 * H + j] = from_f32<T>(gg);
+      grow[3 * H + j] = from_f32<T>(go);
+      c_reg[ts] = c;
+      h_reg[ts] = h;
+    }
+    xsignal(y, local);  // its barrier also orders this step's LDS use before the next
+    off_prev = off;
+    off += nb;
+  }
+}
+
+// ---------------------------------------------------------------- backward --
+// dh_rec[rows][units] = dA_{t+1}[rows][4H] W_h[4H][units]: output tiles of
+// 16 units (the last one partly empty), k-range split over the 4 waves.
+// MT: row tiles; NTU: unit tiles; KPW: k-steps per wave (4H = 128 KPW).
+template <typename T, int MT, int NTU, int KPW>
+__global__ __launch_bounds__(256, 1) void lstm_bwd_xcd(PersistBwd a, PersistSchedule ps, XcdSync y) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  Frag<T>* wl = reinterpret_cast<Frag<T>*>(lds);                  // [n][ks][lane]
+  f32x4_t* red = reinterpret_cast<f32x4_t*>(lds + BWD_LDS_W);      // [wave][m][lane] per unit tile
+  __shared__ int bad_sh;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int H = a.hidden, G4 = 4 * H, U = y.units;
+  const int ksteps = G4 / 32;
+  const int blk = blockIdx.x % NX, us = blockIdx.x / NX;
+  const int b0 = blk * 16 * MT, j0 = us * U;
+  const int members = H / U;
+  const int koct = (lane >> 4) * 8;
+  const T* __restrict__ Wh = static_cast<const T*>(a.Wh);
+  const T* __restrict__ dHa = static_cast<const T*>(a.dHa);
+  const T* __restrict__ Gb = static_cast<const T*>(a.G);
+  T* __restrict__ dA = static_cast<T*>(a.dA);
+
+  // W_h^T fragments of unit tile n (vc_n = min(16, U - 16n) valid columns),
+  // k-step ks: W_h[k .. k+7][j0 + 16n + c] for c < vc_n, stored compactly at
+  // base(n) + ks * 4 vc_n + (k-octet) vc_n + c with base(n) = 64 ksteps n.
+  for (int n = 0; n < NTU; ++n) {
+    const int vc = min(16, U - 16 * n);
+    for (int e = threadIdx.x; e < ksteps * 4 * vc; e += 256) {
+      const int c = e % vc, oct = (e / vc) & 3, ks = e / (4 * vc);
+      const int k = ks * 32 + oct * 8;
+      T v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = Wh[(int64_t)(k + q) * H + j0 + 16 * n + c];
+      Frag<T> f;
+      memcpy(&f, v, sizeof f);
+      wl[64 * ksteps * n + e] = f;
+    }
+  }
+  const bool local = check_local(y, &bad_sh);
+
+  // finishing tile of this wave: row tile wave % MT, unit tile wave / MT
+  const int fm = wave % MT, fn = wave / MT;
+  const bool fin = fn < NTU;
+  const int uu = 16 * fn + (lane & 15);              // unit within the slice
+  const bool uok = fin && uu < U;
+  const int j = j0 + (uok ? uu : 0);
+  float dc_reg[4] = {0.f, 0.f, 0.f, 0.f};
+
+  int nb = ps.T > 0 ? active_up(ps, 0, ps.T - 1) : 0;
+  int off = ps.N - nb;
+  int nb_next = 0, off_next = 0;
+  unsigned done = 0;
+  for (int t = ps.T - 1; t >= 0; --t) {
+    if (t < ps.T - 1) {
+      nb_next = nb;
+      off_next = off;
+      nb = active_up(ps, nb_next, t);
+      off = off_next - nb;
+    }
+    if (b0 >= nb) continue;
+    const int nb_prev = t > 0 ? active_up(ps, nb, t - 1) : 0;
+    const int off_prev = off - nb_prev;
+
+    T gv[4][4], dhv[4];
+    float cv[4], cpv[4];
+    const float* cprev_rows = t > 0 ? a.C + (int64_t)off_prev * H : a.c0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int b = min(b0 + fm * 16 + mfma_row(lane, r), nb - 1);
+      const int64_t o = (int64_t)(off + b) * H + j;
+      const T* grow = Gb + (int64_t)(off + b) * G4;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) gv[r][g] = grow[g * H + j];
+      cv[r] = a.C[o];
+      cpv[r] = cprev_rows[(int64_t)b * H + j];
+      dhv[r] = dHa[o];
+    }
+
+    f32x4_t acc[MT][NTU];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int n = 0; n < NTU; ++n) acc[m][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (b0 < nb_next) {
+      xwait(y, local, (unsigned)members * done);
+      const T* dAn = dA + (int64_t)off_next * G4;
+      const T* arow[MT];
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+        arow[m] = dAn + (int64_t)min(b0 + m * 16 + (lane & 15), nb_next - 1) * G4 + koct;
+      constexpr int PH = (MT * KPW > 24) ? (24 / MT) : KPW;  // k-steps per batch of loads
+#pragma unroll
+      for (int s0 = 0; s0 < KPW; s0 += PH) {
+        Frag<T> af[PH][MT];
+#pragma unroll
+        for (int s = 0; s < PH; ++s)
+#pragma unroll
+          for (int m = 0; m < MT; ++m) {
+            const int ks = wave + 4 * (s0 + s);
+            af[s][m] = frag_load<T>(arow[m] + (s0 + s < KPW && ks < ksteps ? ks * 32 : 0));
+          }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int s = 0; s < PH; ++s) {
+          const int ks = wave + 4 * (s0 + s);
+          if (s0 + s >= KPW || ks >= ksteps) break;
+#pragma unroll
+          for (int n = 0; n < NTU; ++n) {
+            // lanes past the tile's valid columns read a valid entry; their
+            // output columns are never used
+            const int vc = min(16, U - 16 * n);
+            const Frag<T> bf =
+                wl[64 * ksteps * n + ks * 4 * vc + (lane >> 4) * vc + min(lane & 15, vc - 1)];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) mma_16x16x32(acc[m][n], af[s][m], bf);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // fixed-order sum over the 4 waves, one unit tile at a time
+    f32x4_t rec = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int n = 0; n < NTU; ++n) {
+#pragma unroll
+      for (int m = 0; m < MT; ++m) red[(wave * MT + m) * 64 + lane] = acc[m][n];
+      __syncthreads();
+      if (fn == n) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) rec += red[(v * MT + fm) * 64 + lane];
+      }
+      __syncthreads();
+    }
+
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int b = b0 + fm * 16 + mfma_row(lane, r);
+      if (!uok || b >= nb) continue;
+      const bool cont = b < nb_next;
+      const float vi = to_f32<T>(gv[r][0]), vf = to_f32<T>(gv[r][1]);
+      const float vg = to_f32<T>(gv[r][2]), vo = to_f32<T>(gv[r][3]);
+      const float dhh = to_f32<T>(dhv[r]) + (cont ? rec[r] : 0.f);
+      const float tc = tanh_f(cv[r]);
+      const float d_o = dhh * tc;
+      const float dcell = dhh * vo * (1.f - tc * tc) + (cont ? dc_reg[r] : 0.f);
+      const float d_i = dcell * vg, d_g = dcell * vi, d_f = dcell * cpv[r];
+      dc_reg[r] = dcell * vf;
+      T* arow = dA + (int64_t)(off + b) * G4;
+      arow[j] = from_f32<T>(d_i * vi * (1.f - vi));
+      arow[H + j] = from_f32<T>(d_f * vf * (1.f - vf));
+      arow[2 * H + j] = from_f32<T>(d_g * (1.f - vg * vg));
+      arow[3 * H + j] = from_f32<T>(d_o * vo * (1.f - vo));
+    }
+    xsignal(y, local);
+    ++done;
+  }
+}
+
+// ------------------------------------------------------------------ launch --
+
+int xcd_units(int H) {
+  // workgroups per XCD = H / U <= 32, U a multiple of 4
+  for (int U = 4; U <= H; U += 4)
+    if (H % U == 0 && H / U <= 32) return U;
+  return 0;
+}
+
+bool fits(const void* fn, int blocks, size_t lds) {
+  int dev = 0, cus = 0, per = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return false;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, 256, lds) != hipSuccess) return false;
+  return per > 0 && blocks <= per * cus;
+}
+
+template <typename K>
+hipError_t coop(K kernel, int blocks, size_t lds, void** args, hipStream_t s, bool* used) {
+  const void* fn = reinterpret_cast<const void*>(kernel);
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess ||
+      !fits(fn, blocks, lds)) {
+    (void)hipGetLastError();
+    *used = false;
+    return hipSuccess;
+  }
+  *used = true;
+  return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(256), args, (unsigned)lds, s);
+}
+
+// Shapes covered: bf16 (the resident slices are sized for it), RB = 16 or
+// 32 sequences per block (B <= 256), hidden sizes with H % 32 == 0 and
+// 4U x H x 2 bytes of forward weights within the LDS budget.
+struct XShape {
+  int MT, KS, U, NT, TPW, NTU, KPW;
+  bool ok;
+};
+
+XShape xshape(int H, int B) {
+  XShape x{};
+  x.ok = false;
+  if (H % 32 != 0 || B > 256 || B < 1) return x;
+  x.MT = B > 128 ? 2 : 1;
+  x.KS = H / 32;
+  x.U = xcd_units(H);
+  if (x.U == 0) return x;
+  x.NT = x.U / 4;
+  x.TPW = (x.MT * x.NT + 3) / 4;
+  x.NTU = (x.U + 15) / 16;
+  x.KPW = (4 * H / 32 + 3) / 4;
+  const int64_t wf = (int64_t)x.NT * x.KS * 64 * 16;
+  const int64_t wb = (int64_t)(4 * H / 32) * 4 * x.U * 16;
+  x.ok = wf <= FWD_LDS_W && wb <= BWD_LDS_W && x.TPW <= 3 && x.NTU <= 2;
+  return x;
+}
+
+}  // namespace
+
+#define AM_FWD_CASE(MT_, KS_, TPW_)                                                      \
+  if (x.MT == MT_ && x.KS == KS_ && x.TPW == TPW_)                                       \
+    return coop(lstm_fwd_xcd<bf16_t, MT_, KS_, TPW_>, blocks, lds, args, s, used);
+
+hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used) {
+  *used = false;
+  const XShape x = xshape(a.hidden, ps.B);
+  if (!x.ok) return hipSuccess;
+  y.units = x.U;
+  const int blocks = NX * (a.hidden / x.U);
+  const size_t lds = FWD_LDS_W + 4 * x.TPW * 64 * 16;
+  void* args[] = {&a, &ps, &y};
+  // instantiated shapes: H = 768 (B <= 128 and <= 256), H = 64, 128
+  AM_FWD_CASE(2, 24, 3) AM_FWD_CASE(1, 24, 2)
+  AM_FWD_CASE(2, 2, 1) AM_FWD_CASE(1, 2, 1)
+  AM_FWD_CASE(2, 4, 1) AM_FWD_CASE(1, 4, 1)
+  return hipSuccess;
+}
+
+#define AM_BWD_CASE(MT_, NTU_, KPW_)                                                     \
+  if (x.MT == MT_ && x.NTU == NTU_ && x.KPW == KPW_)                                     \
+    return coop(lstm_bwd_xcd<bf16_t, MT_, NTU_, KPW_>, blocks, lds, args, s, used);
+
+hipError_t lstm_bwd_xcd_launch(PersistBwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used) {
+  *used = false;
+  const XShape x = xshape(a.hidden, ps.B);
+  if (!x.ok) return hipSuccess;
+  y.units = x.U;
+  const int blocks = NX * (a.hidden / x.U);
+  const size_t lds = BWD_LDS_W + 4 * x.MT * 64 * 16;
+  void* args[] = {&a, &ps, &y};
+  AM_BWD_CASE(2, 2, 24) AM_BWD_CASE(1, 2, 24)
+  AM_BWD_CASE(2, 1, 2) AM_BWD_CASE(1, 1, 2)
+  AM_BWD_CASE(2, 1, 4) AM_BWD_CASE(1, 1, 4)
+  return hipSuccess;
+}
+
+bool lstm_xcd_instantiated(bool forward, int hidden, int B) {
+  const XShape x = xshape(hidden, B);
+  if (!x.ok) return false;
+  if (forward)
+    return (x.KS == 24 && ((x.MT == 2 && x.TPW == 3) || (x.MT == 1 && x.TPW == 2))) ||
+           ((x.KS == 2 || x.KS == 4) && x.TPW == 1);
+  return (x.KPW == 24 && x.NTU == 2) || ((x.KPW == 2 || x.KPW == 4) && x.NTU == 1);
+}
+
+}  // namespace am

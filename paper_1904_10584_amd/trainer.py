@@ -81,6 +81,11 @@ class StudentStep:
             upd = self.grads
         am.sgd_apply(self.master, upd, self.lr, self.weights)
 
+    def check(self):
+        """Synchronise; raise if a recurrence step barrier of the last pass
+        timed out (the pass's outputs are then invalid)."""
+        am.workspace_check(self.ws)
+
     def step(self):
         self.forward()
         self.loss_and_grad()

@@ -71,6 +71,7 @@ def gpu_forward_backward(m, master, x, T, B, idx, prob, lengths=None, h0=None, c
             dz = dz.to(torch.bfloat16)
     grads = torch.empty(am.param_count(m), dtype=torch.float32, device="cuda")
     am.lstm_am_backward(m, params, xd, T, B, dz, ws, grads, lengths=lengths)
+    am.workspace_check(ws)
     torch.cuda.synchronize()
     out["logits"] = logits.cpu().numpy()
     out["dlogits"] = dz.float().cpu().numpy()

@@ -119,8 +119,16 @@ def test_encode_decode_ce_sgd_argument_checks(L):
     assert st == -1
     st, _ = _status(L, "sgd_apply", -1, fake, None, fake, ctypes.c_float(0.1), None)
     assert st == -1
-    for s in (0, -1, -2, -3, -4, -5):
+    for s in (0, -1, -2, -3, -4, -5, -6):
         assert L.am_status_string(s)
+    assert b"timed out" in L.am_status_string(-6)
+    # the time-out query validates before it touches the stream
+    st, _ = _status(L, "am_workspace_check", None, 1 << 20, None)
+    assert st == -1
+    st, _ = _status(L, "am_workspace_check", ctypes.c_void_p(0x100010), 1 << 20, None)
+    assert st == -1   # not 256-byte aligned
+    st, _ = _status(L, "am_workspace_check", fake, 4096, None)
+    assert st == -5   # smaller than the sync region
 
 
 def test_workspace_queries_are_monotone(L):

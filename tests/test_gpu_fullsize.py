@@ -72,6 +72,7 @@ def _sampled_check(name, sample):
     dz_sub[rows] = dz_gpu[rows]
     st.dlogits.copy_(torch.from_numpy(dz_sub).to(torch.bfloat16).cuda())
     st.backward()
+    st.check()
     torch.cuda.synchronize()
     grads = st.grads.cpu().numpy()
 
@@ -120,6 +121,7 @@ def test_threshold_compression_100_steps_bit_exact():
         st.forward()
         st.loss_and_grad()
         st.backward()
+        st.check()
         torch.cuda.synchronize()
         g = st.grads.cpu().numpy()
         st.apply()

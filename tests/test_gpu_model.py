@@ -18,14 +18,16 @@ F32_TOL = 1e-4
 BF16_TOL = 2e-2
 
 
-@pytest.fixture(params=["persistent", "single_step"], autouse=True)
+@pytest.fixture(params=["auto", "device", "step"], autouse=True)
 def recurrence_path(request, monkeypatch):
-    """Every test runs with the persistent layer kernels and again with one
-    launch per time step."""
-    if request.param == "single_step":
-        monkeypatch.setenv("AM_STEP_KERNELS", "1")
+    """Every test runs with the default recurrence kernels (XCD-local where
+    the shape is covered), with the device-scope persistent kernels, and
+    with one launch per time step."""
+    monkeypatch.delenv("AM_STEP_KERNELS", raising=False)
+    if request.param == "auto":
+        monkeypatch.delenv("AM_RECURRENCE", raising=False)
     else:
-        monkeypatch.delenv("AM_STEP_KERNELS", raising=False)
+        monkeypatch.setenv("AM_RECURRENCE", request.param)
     return request.param
 
 
