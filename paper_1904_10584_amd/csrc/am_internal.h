@@ -30,6 +30,12 @@ struct GemmArgs {
   float* ws = nullptr; int64_t ws_floats = 0;
 };
 hipError_t gemm(const GemmArgs& g, hipStream_t s);
+// The bf16 products (gemm routes bf16 arguments here).
+hipError_t gemm_bf16(const GemmArgs& g, hipStream_t s);
+// Sum of S split-K partial results [S][M][N] (and partial row sums [S][M])
+// into g.C / g.C2 (and g.rowsum), in split order.
+hipError_t splitk_reduce_launch(const float* part, int S, const GemmArgs& g, const float* rs_part,
+                                hipStream_t s);
 
 // One forward step of one LSTM layer over the nb active rows of step t:
 // gate pre-activations P (input projection + bias, rows of step t) plus

@@ -1,25 +1,25 @@
-// MFMA GEMM family for the batched products of the training step:
+// fp32 MFMA GEMM family (the fp32 model path; bf16 products are in
+// gemm_bf16.hip):
 //   forward projections  P = X Wx^T + b,  Z = H Wo^T + bo      (NT, bias)
 //   data gradients       dH = dZ Wo,  dX = dA Wx              (NN)
 //   weight gradients     [dWx | dWh] = dA^T [X | Hs],  dWo = dZ^T H   (TN)
 // One 256-thread workgroup computes a 128x128 tile; its four waves each own a
-// 64x64 quadrant as 4x4 MFMA 16x16 tiles (16x16x32 bf16, or 8 x 16x16x4
-// fp32 per 32-wide k-step).  Operands are staged in LDS as [row][k] with a
-// 16-byte pad per row.  A k-major operand is copied with 16-byte loads; an
-// m/n-major one (the TN and NN cases) is loaded as 8(k) x 4(m) blocks that
-// each thread transposes in registers, so every LDS tile is k-contiguous and
-// the fragment reads are single 16-byte LDS loads.  Global loads for tile
-// k+1 are issued before the MFMAs of tile k (double-buffered LDS, one
-// barrier per k-tile).
+// 64x64 quadrant as 4x4 MFMA 16x16 tiles (8 x 16x16x4 fp32 per 32-wide
+// k-step).  Operands are staged in LDS as [row][k] with a 16-byte pad per
+// row.  A k-major operand is copied with 16-byte loads; an m/n-major one (the
+// TN and NN cases) is loaded as 4(k) x 4(m) blocks that each thread
+// transposes in registers, so every LDS tile is k-contiguous.  Global loads
+// for tile k+1 are issued before the MFMAs of tile k (double-buffered LDS,
+// one barrier per k-tile).
 //
-// Weight gradients reduce over all frames (K up to ~10^5) into a small
-// output, so they split K over workgroups: each split writes an fp32 partial
-// tile to the workspace and a second kernel adds the partials in split order
-// (deterministic; no atomics).  The same pass yields the bias gradient:
-// while loading the A tile (dA or dZ, m-major) each thread keeps the sums of
-// its 4 rows over its k-rows, and the first column of tiles writes them.
-// The B operand of the TN product may come from two matrices side by side
-// (X and the shifted hidden states), so dWx and dWh are one launch.
+// Weight gradients reduce over all frames into a small output, so they split
+// K over workgroups: each split writes an fp32 partial tile to the workspace
+// and splitk_reduce adds the partials in split order (deterministic; no
+// atomics).  The same pass yields the bias gradient: while loading the A tile
+// (dA or dZ, m-major) each thread keeps the sums of its 4 rows over its
+// k-rows, and the first column of tiles writes them.  The B operand of the TN
+// product may come from two matrices side by side (X and the shifted hidden
+// states), so dWx and dWh are one launch.
 #include "am_device.h"
 #include "am_internal.h"
 
@@ -30,7 +30,6 @@ constexpr int TB = 128;   // tile rows and columns
 constexpr int NT = 256;   // threads per workgroup
 
 template <typename T> struct KT;
-template <> struct KT<bf16_t> { static constexpr int BK = 64, VEC = 8; };
 template <> struct KT<float>  { static constexpr int BK = 32, VEC = 4; };
 
 template <typename T> struct Tile {
@@ -78,57 +77,6 @@ template <typename T> struct Loader<T, true> {
   }
   __device__ void rowsum_init() {}
   __device__ float rowsum(int) const { return 0.f; }
-};
-
-// m/n-major, bf16: thread (kb, mb) loads 8 k-rows x 4 rows-of-the-tile and
-// transposes them into 4 k-octets.  Optionally sums its 4 rows over k.
-template <> struct Loader<bf16_t, false> {
-  uint4 reg[4];
-  float rs[4];
-  __device__ void rowsum_init() { rs[0] = rs[1] = rs[2] = rs[3] = 0.f; }
-  __device__ float rowsum(int q) const { return rs[q]; }
-  template <bool SUM = false>
-  __device__ void load(const Src<bf16_t>& s, int row0, int nrows, int k0, int kend) {
-    const int kb = threadIdx.x >> 5, mb = threadIdx.x & 31;
-    const int m = row0 + mb * 4;
-    const bool second = m >= s.split;
-    const bf16_t* base = second ? s.p1 : s.p0;
-    const int64_t ld = second ? s.ld1 : s.ld0;
-    const int mm = second ? m - s.split : m;
-    uint2 in[8];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      int k = k0 + kb * 8 + r;
-      if (k < kend && m < nrows)
-        in[r] = *reinterpret_cast<const uint2*>(base + (int64_t)k * ld + mm);
-      else
-        in[r] = make_uint2(0, 0);
-    }
-    // element q of row r: q=0 low half of .x, 1 high half of .x, 2/3 in .y
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      uint32_t w[8];
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        uint32_t d = (q < 2) ? in[r].x : in[r].y;
-        w[r] = (q & 1) ? (d >> 16) : (d & 0xFFFFu);
-      }
-      if (SUM) {
-        float acc = 0.f;
-#pragma unroll
-        for (int r = 0; r < 8; ++r) acc += bf16_to_f32((bf16_t)w[r]);
-        rs[q] += acc;
-      }
-      reg[q] = make_uint4(w[0] | (w[1] << 16), w[2] | (w[3] << 16),
-                          w[4] | (w[5] << 16), w[6] | (w[7] << 16));
-    }
-  }
-  __device__ void store(bf16_t* lds) {
-    int kb = threadIdx.x >> 5, mb = threadIdx.x & 31;
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      *reinterpret_cast<uint4*>(lds + (mb * 4 + q) * Tile<bf16_t>::LDK + kb * 8) = reg[q];
-  }
 };
 
 // m/n-major, fp32: 4 k-rows x 4 rows-of-the-tile per thread.
@@ -382,22 +330,27 @@ hipError_t dispatch(const GemmArgs& g, hipStream_t s) {
     Dst<float> d{part, g.N, part, g.N, 1 << 30, (int64_t)g.M * g.N};  // one slice per split
     if (g.rowsum) launch<T, false, false, float, false, true>(g, d, rs_part, S, kps, s);
     else launch<T, false, false, float, false, false>(g, d, nullptr, S, kps, s);
-    const int64_t nq = (int64_t)g.M * g.N / 4;
-    const int64_t threads = nq + (g.rowsum ? g.M : 0);
-    hipLaunchKernelGGL(splitk_reduce, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, part,
-                       S, g.M, g.N, static_cast<float*>(g.C), g.ldc,
-                       static_cast<float*>(g.C2 ? g.C2 : g.C), g.C2 ? g.ldc2 : g.ldc,
-                       g.C2 ? g.n_split : (1 << 30), rs_part, g.rowsum);
-    return hipGetLastError();
+    return splitk_reduce_launch(part, S, g, rs_part, s);
   }
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
+hipError_t splitk_reduce_launch(const float* part, int S, const GemmArgs& g, const float* rs_part,
+                                hipStream_t s) {
+  const int64_t nq = (int64_t)g.M * g.N / 4;
+  const int64_t threads = nq + (g.rowsum ? g.M : 0);
+  hipLaunchKernelGGL(splitk_reduce, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, part,
+                     S, g.M, g.N, static_cast<float*>(g.C), g.ldc,
+                     static_cast<float*>(g.C2 ? g.C2 : g.C), g.C2 ? g.ldc2 : g.ldc,
+                     g.C2 ? g.n_split : (1 << 30), rs_part, g.rowsum);
+  return hipGetLastError();
+}
+
 hipError_t gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
-  return g.bf16 ? dispatch<bf16_t>(g, s) : dispatch<float>(g, s);
+  return g.bf16 ? gemm_bf16(g, s) : dispatch<float>(g, s);
 }
 
 }  // namespace am
