@@ -92,6 +92,27 @@ __device__ __forceinline__ float sigm(float x) {
 }
 __device__ __forceinline__ float tanh_f(float x) { return 2.0f * sigm(2.0f * x) - 1.0f; }
 
+// Byte address of an LDS object (for instructions that take it in M0).
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+// 16 bytes per lane from global memory straight to LDS at lds_base + 16 *
+// lane (global_load_lds_dwordx4; lds_base is wave-uniform).  On gfx950 this
+// moves about 2.5x the bytes per CU per clock of loads into VGPRs.  The load
+// is counted by vmcnt and is invisible to the compiler's wait insertion, so
+// the caller waits explicitly (wait_vm) before the data is read.
+__device__ __forceinline__ void dma16(const void* src, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(lds_base) : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N), other counters untouched.
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

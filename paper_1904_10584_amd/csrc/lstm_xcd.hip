@@ -18,9 +18,9 @@
 //     so no consumer's L1 can hold a stale copy.
 // A workgroup owns U hidden units (U % 4 == 0) of one block of RB sequences
 // (RB = 16 or 32).  The forward product keeps the workgroup's 4U columns of
-// W_h resident in LDS in unit-major, gate-minor order, so a 16-column MFMA
-// tile holds 4 units x 4 gates; a per-wave transpose of 4x4 quads through
-// LDS then gives each lane all four gate pre-activations of one
+// W_h resident in registers in unit-major, gate-minor order, so a 16-column
+// MFMA tile holds 4 units x 4 gates; a per-wave transpose of 4x4 quads
+// through LDS then gives each lane all four gate pre-activations of one
 // (sequence, unit).  The backward product keeps the U rows of W_h^T in LDS.
 #include "am_device.h"
 #include "am_internal.h"
@@ -30,7 +30,6 @@ namespace {
 
 constexpr int NX = 8;                    // XCDs
 constexpr unsigned SPIN_LIMIT = 1u << 22;
-constexpr int FWD_LDS_W = 147456;        // bytes of resident weights, forward
 constexpr int BWD_LDS_W = 147456;        // bytes of resident weights, backward
 
 __device__ __forceinline__ unsigned xcc_id() {
@@ -113,52 +112,79 @@ __device__ __forceinline__ int active_up(const PersistSchedule& ps, int nb, int 
 }
 
 // ----------------------------------------------------------------- forward --
-// MT: row tiles (RB = 16 MT); KS: k-steps (H = 32 KS); TPW: output tiles per wave.
-template <typename T, int MT, int KS, int TPW>
-__global__ __launch_bounds__(256, 1) void lstm_fwd_xcd(PersistFwd a, PersistSchedule ps, XcdSync y) {
+// Eight waves, two per SIMD (one wave per SIMD issues MFMAs at half the
+// rate two can).  Tile group g = wave % 4 owns the output tiles t = g + 4 ts
+// (row tile t % MT, column tile t / MT; all tiles of a group share row tile
+// g % MT); k-half kh = wave / 4 multiplies k-steps [kh KS/2, (kh+1) KS/2).
+// The W_h fragments of a wave's tiles and k-steps stay in its registers for
+// the whole launch.  Each step the block's rows of h_{t-1} are copied to
+// LDS with direct loads (whole 128-byte lines), laid out line-major
+// [H/64 lines][RB rows][128 B] with the 16-byte chunks of a row XOR-swizzled
+// by row, and read back as MFMA fragments.  The two k-halves of a group swap
+// partial tiles through LDS: the k-half-0 wave finishes the first
+// ceil(TPW/2) tiles, the k-half-1 wave the rest.  A step is signalled as soon
+// as its h stores (the only exchanged data) are complete; the cell state,
+// gate and h_{t-1} copies are stored after the signal.
+template <int MT, int KS, int TPW>
+__global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSchedule ps, XcdSync y) {
+  constexpr int RB = 16 * MT;             // sequences per block
+  constexpr int KH = KS / 2;              // k-steps per wave
+  constexpr int FIN = (TPW + 1) / 2;      // tiles finished by the k-half-0 wave
+  constexpr int HS_BYTES = RB * KS * 64;  // the block's h rows: RB x H bf16
+  static_assert(KS % 2 == 0, "H must be a multiple of 64");
   extern __shared__ __align__(16) unsigned char lds[];
-  Frag<T>* wl = reinterpret_cast<Frag<T>*>(lds);                       // [n][s][lane]
-  f32x4_t* xs = reinterpret_cast<f32x4_t*>(lds + FWD_LDS_W);            // [wave][tile][lane]
+  bf16_t* hl = reinterpret_cast<bf16_t*>(lds);
+  f32x4_t* red = reinterpret_cast<f32x4_t*>(lds + HS_BYTES);  // [8][TPW][64]
+  f32x4_t* xs = red + 8 * TPW * 64;                             // [8][TPW][64]
   __shared__ int bad_sh;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int H = a.hidden, G4 = 4 * H, U = y.units;
-  const int NT = U / 4;                        // 16-column tiles = 4 units x 4 gates
-  const int ntiles = MT * NT;
+  const int g = wave & 3, kh = wave >> 2;
+  const int H = KS * 32, G4 = 4 * H, U = y.units;
+  const int ntiles = MT * (U / 4);
   const int blk = blockIdx.x % NX, us = blockIdx.x / NX;
-  const int b0 = blk * 16 * MT, j0 = us * U;
+  const int b0 = blk * RB, j0 = us * U;
   const int members = H / U;
-  const int koct = (lane >> 4) * 8;
-  const T* __restrict__ P = static_cast<const T*>(a.P);
-  const T* __restrict__ Wh = static_cast<const T*>(a.Wh);
-  const T* __restrict__ h0 = static_cast<const T*>(a.h0);
-  T* __restrict__ Hb = static_cast<T*>(a.H);
-  T* __restrict__ Hs = static_cast<T*>(a.Hs);
-  T* __restrict__ Gb = static_cast<T*>(a.G);
+  const int mw = g % MT;
+  const int ts_lo = kh == 0 ? 0 : FIN, ts_hi = kh == 0 ? FIN : TPW;
+  const bf16_t* __restrict__ P = static_cast<const bf16_t*>(a.P);
+  const bf16_t* __restrict__ Wh = static_cast<const bf16_t*>(a.Wh);
+  const bf16_t* __restrict__ h0 = static_cast<const bf16_t*>(a.h0);
+  bf16_t* __restrict__ Hb = static_cast<bf16_t*>(a.H);
+  bf16_t* __restrict__ Hs = static_cast<bf16_t*>(a.Hs);
+  bf16_t* __restrict__ Gb = static_cast<bf16_t*>(a.G);
 
   // resident weights: column c of tile n is unit j0 + 4n + c/4, gate c%4
-  for (int e = threadIdx.x; e < NT * KS * 64; e += 256) {
-    const int l = e & 63, s = (e >> 6) % KS, n = e / (64 * KS);
-    const int c = l & 15, k = s * 32 + (l >> 4) * 8;
+  Frag<bf16_t> wf[TPW][KH];
+#pragma unroll
+  for (int ts = 0; ts < TPW; ++ts) {
+    const int t = g + 4 * ts;
+    const int n = (t < ntiles ? t : 0) / MT;
+    const int c = lane & 15;
     const int row = (c & 3) * H + j0 + 4 * n + (c >> 2);
-    wl[e] = k < H ? frag_load<T>(Wh + (int64_t)row * H + k) : frag_zero<T>();
+#pragma unroll
+    for (int s = 0; s < KH; ++s)
+      wf[ts][s] = frag_load<bf16_t>(Wh + (int64_t)row * H + (kh * KH + s) * 32 + (lane >> 4) * 8);
   }
   const bool local = check_local(y, &bad_sh);
 
-  // the lane's cells: tile t = wave + 4 ts -> row tile t % MT, column tile t / MT;
-  // row m*16 + 4(lane/16) + lane%4, unit j0 + 4n + (lane%16)/4
-  const int mw = wave % MT;
+  // The tiles this wave finishes ("own slots" o < FIN): tile index
+  // ts = o (k-half 0) or FIN + o (k-half 1).  The lane's cells in tile t:
+  // row mw*16 + 4(lane/16) + lane%4 of the block, unit j0 + 4(t/MT) + (lane%16)/4.
   const int qrow = mw * 16 + 4 * (lane >> 4) + (lane & 3);
-  float c_reg[TPW];
-  T h_reg[TPW];
+  auto slot_ts = [&](int o) { return kh == 0 ? o : FIN + o; };
+  auto slot_ok = [&](int o) { return slot_ts(o) < TPW && g + 4 * slot_ts(o) < ntiles; };
+  auto unit = [&](int o) {
+    const int t = g + 4 * slot_ts(o);
+    return j0 + 4 * ((t < ntiles ? t : 0) / MT) + ((lane & 15) >> 2);
+  };
+  float c_reg[FIN];
+  bf16_t h_reg[FIN];
 #pragma unroll
-  for (int ts = 0; ts < TPW; ++ts) {
-    const int t = wave + 4 * ts;
-    const int j = j0 + 4 * (t / MT) + ((lane & 15) >> 2);
-    const int b = b0 + qrow;
-    const bool ok = t < ntiles && b < ps.B;
-    c_reg[ts] = ok ? a.c0[(int64_t)b * H + j] : 0.f;
-    h_reg[ts] = (ok && h0) ? h0[(int64_t)b * H + j] : from_f32<T>(0.f);
+  for (int o = 0; o < FIN; ++o) {
+    const int b = min(b0 + qrow, ps.B - 1), j = unit(o);
+    c_reg[o] = a.c0[(int64_t)b * H + j];
+    h_reg[o] = h0 ? h0[(int64_t)b * H + j] : (bf16_t)0;
   }
 
   int nb = ps.B, off = 0, off_prev = 0;
@@ -166,79 +192,115 @@ __global__ __launch_bounds__(256, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
     nb = active_down(ps, nb, t);
     if (b0 >= nb) break;  // this block of sequences has ended for good
 
-    T pin[TPW][4];
+    // input projections of this lane's cells (independent of the exchange;
+    // clamped, unmasked loads so that they issue back to back)
+    bf16_t pin[FIN][4];
+    const bf16_t* prow = P + (int64_t)(off + min(b0 + qrow, nb - 1)) * G4;
 #pragma unroll
-    for (int ts = 0; ts < TPW; ++ts) {
-      const int tt = wave + 4 * ts;
-      const int j = j0 + 4 * ((tt < ntiles ? tt : 0) / MT) + ((lane & 15) >> 2);
-      const T* prow = P + (int64_t)(off + min(b0 + qrow, nb - 1)) * G4;
+    for (int o = 0; o < FIN; ++o)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) pin[ts][g] = prow[g * H + j];
-    }
+      for (int q = 0; q < 4; ++q) pin[o][q] = prow[q * H + unit(o)];
 
     f32x4_t acc[TPW];
 #pragma unroll
     for (int ts = 0; ts < TPW; ++ts) acc[ts] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    const T* hprev = h0;
+    const bf16_t* hsrc = h0;
     if (t > 0) {
       xwait(y, local, (unsigned)(members * t));
-      hprev = Hb + (int64_t)off_prev * H;
+      hsrc = Hb + (int64_t)off_prev * H;
     }
-    if (hprev) {
-      // all of the wave's A fragments in flight at once (clamped, unmasked)
-      const T* hrow = hprev + (int64_t)min(b0 + mw * 16 + (lane & 15), nb - 1) * H + koct;
-      Frag<T> af[KS];
+    if (hsrc) {
+      // the block's rows of h_{t-1} (inactive rows read an active one) to LDS
+      constexpr int RG = RB / 8, NQ = (KS / 2) * RG;
+      for (int q = wave; q < NQ; q += 8) {
+        const int line = q / RG, rg = q % RG;
+        const int r = rg * 8 + (lane >> 3);
+        const int chunk = line * 8 + ((lane & 7) ^ (r & 7));
+        dma16(hsrc + (int64_t)min(b0 + r, nb - 1) * H + chunk * 8,
+              __builtin_amdgcn_readfirstlane(lds_address(hl + (line * RB + rg * 8) * 64)));
+      }
+      wait_vm<0>();
+      __syncthreads();
+      // A fragments in batches of up to four, each batch read before its
+      // MFMAs (the resident weights leave room for four in registers)
+      constexpr int AB = KH > 4 ? 4 : KH;
+      const int r = mw * 16 + (lane & 15);
 #pragma unroll
-      for (int s = 0; s < KS; ++s) af[s] = frag_load<T>(hrow + (s * 32 + koct < H ? s * 32 : 0));
-      __builtin_amdgcn_sched_barrier(0);
+      for (int s0 = 0; s0 < KH; s0 += AB) {
+        Frag<bf16_t> af[AB];
 #pragma unroll
-      for (int ts = 0; ts < TPW; ++ts) {
-        const int tt = wave + 4 * ts;
-        if (tt >= ntiles) break;
-        const Frag<T>* wn = wl + (tt / MT) * KS * 64 + lane;
+        for (int s = 0; s < AB; ++s) {
+          const int c = (kh * KH + s0 + s) * 4 + (lane >> 4);
+          af[s] = *reinterpret_cast<const Frag<bf16_t>*>(
+              hl + ((c >> 3) * RB + r) * 64 + (((c & 7) ^ (r & 7)) << 3));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // unconditional: a tile past the last holds tile 0's weights and its
+        // result is never used (a guard here would branch around each MFMA)
 #pragma unroll
-        for (int s = 0; s < KS; ++s) mma_16x16x32(acc[ts], af[s], wn[s * 64]);
+        for (int s = 0; s < AB; ++s)
+#pragma unroll
+          for (int ts = 0; ts < TPW; ++ts) mma_16x16x32(acc[ts], af[s], wf[ts][s0 + s]);
       }
     }
 
-    // 4x4 quad transpose: lane l gets, for row 4(l/16) + l%4, the 4 gates
-    // of its unit from lanes (l & ~3) + g
-    f32x4_t* xw = xs + wave * TPW * 64;
-#pragma unroll
-    for (int ts = 0; ts < TPW; ++ts) xw[ts * 64 + lane] = acc[ts];
-    float gpre[TPW][4];
+    // the k-halves of the group swap the partial tiles the other finishes
 #pragma unroll
     for (int ts = 0; ts < TPW; ++ts)
+      if (!(ts >= ts_lo && ts < ts_hi)) red[(wave * TPW + ts) * 64 + lane] = acc[ts];
+    __syncthreads();
+    f32x4_t fin[FIN];
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
-        gpre[ts][g] = reinterpret_cast<const float*>(xw + ts * 64 + (lane & ~3) + g)[lane & 3];
+    for (int o = 0; o < FIN; ++o) {
+      const int ts0 = o, ts1 = FIN + o < TPW ? FIN + o : o;  // static candidates
+      fin[o] = kh == 0 ? acc[ts0] : acc[ts1];
+      fin[o] += red[((wave ^ 4) * TPW + slot_ts(o) % TPW) * 64 + lane];
+    }
+
+    // 4x4 quad transpose: lane l gets, for row 4(l/16) + l%4, the 4 gates
+    // of its unit from lanes (l & ~3) + q
+    f32x4_t* xw = xs + wave * TPW * 64;
+#pragma unroll
+    for (int o = 0; o < FIN; ++o) xw[o * 64 + lane] = fin[o];
+    float gate[FIN][4];
+#pragma unroll
+    for (int o = 0; o < FIN; ++o)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        gate[o][q] = reinterpret_cast<const float*>(xw + o * 64 + (lane & ~3) + q)[lane & 3];
 
     const int b = b0 + qrow;
+    const bool row_ok = b < nb;
+    float cnew[FIN];
+    bf16_t hprev[FIN];
 #pragma unroll
-    for (int ts = 0; ts < TPW; ++ts) {
-      const int tt = wave + 4 * ts;
-      if (tt >= ntiles || b >= nb) continue;
-      const int j = j0 + 4 * (tt / MT) + ((lane & 15) >> 2);
-      const float gi = sigm(gpre[ts][0] + to_f32<T>(pin[ts][0]));
-      const float gf = sigm(gpre[ts][1] + to_f32<T>(pin[ts][1]));
-      const float gg = tanh_f(gpre[ts][2] + to_f32<T>(pin[ts][2]));
-      const float go = sigm(gpre[ts][3] + to_f32<T>(pin[ts][3]));
-      const float c = gf * c_reg[ts] + gi * gg;
-      const T h = from_f32<T>(go * tanh_f(c));
-      const int64_t o = (int64_t)(off + b) * H + j;
-      a.C[o] = c;
-      Hb[o] = h;
-      Hs[o] = h_reg[ts];
-      T* grow = Gb + (int64_t)(off + b) * G4;
-      grow[j] = from_f32<T>(gi);
-      grow[H + j] = from_f32<T>(gf);
-      grow[2 * H + j] = from_f32<T>(gg);
-      grow[3 * H + j] = from_f32<T>(go);
-      c_reg[ts] = c;
-      h_reg[ts] = h;
+    for (int o = 0; o < FIN; ++o) {
+      hprev[o] = h_reg[o];
+      gate[o][0] = sigm(gate[o][0] + bf16_to_f32(pin[o][0]));
+      gate[o][1] = sigm(gate[o][1] + bf16_to_f32(pin[o][1]));
+      gate[o][2] = tanh_f(gate[o][2] + bf16_to_f32(pin[o][2]));
+      gate[o][3] = sigm(gate[o][3] + bf16_to_f32(pin[o][3]));
+      cnew[o] = gate[o][1] * c_reg[o] + gate[o][0] * gate[o][2];
+      const bf16_t h = f32_to_bf16(gate[o][3] * tanh_f(cnew[o]));
+      if (row_ok && slot_ok(o)) {
+        Hb[(int64_t)(off + b) * H + unit(o)] = h;
+        c_reg[o] = cnew[o];
+        h_reg[o] = h;
+      }
     }
-    xsignal(y, local);  // its barrier also orders this step's LDS use before the next
+    xsignal(y, local);  // h stores complete; its barrier also orders the LDS reuse
+    // stores only the backward pass reads
+#pragma unroll
+    for (int o = 0; o < FIN; ++o) {
+      if (!row_ok || !slot_ok(o)) continue;
+      const int j = unit(o);
+      const int64_t ofs = (int64_t)(off + b) * H + j;
+      a.C[ofs] = cnew[o];
+      Hs[ofs] = hprev[o];
+      bf16_t* grow = Gb + (int64_t)(off + b) * G4;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) grow[q * H + j] = f32_to_bf16(gate[o][q]);
+    }
     off_prev = off;
     off += nb;
   }
@@ -412,30 +474,32 @@ int xcd_units(int H) {
   return 0;
 }
 
-bool fits(const void* fn, int blocks, size_t lds) {
+bool fits(const void* fn, int blocks, int threads, size_t lds) {
   int dev = 0, cus = 0, per = 0;
   if (hipGetDevice(&dev) != hipSuccess) return false;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return false;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, 256, lds) != hipSuccess) return false;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, threads, lds) != hipSuccess) return false;
   return per > 0 && blocks <= per * cus;
 }
 
 template <typename K>
-hipError_t coop(K kernel, int blocks, size_t lds, void** args, hipStream_t s, bool* used) {
+hipError_t coop(K kernel, int blocks, int threads, size_t lds, void** args, hipStream_t s,
+                bool* used) {
   const void* fn = reinterpret_cast<const void*>(kernel);
   if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess ||
-      !fits(fn, blocks, lds)) {
+      !fits(fn, blocks, threads, lds)) {
     (void)hipGetLastError();
     *used = false;
     return hipSuccess;
   }
   *used = true;
-  return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(256), args, (unsigned)lds, s);
+  return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(threads), args, (unsigned)lds, s);
 }
 
 // Shapes covered: bf16 (the resident slices are sized for it), RB = 16 or
-// 32 sequences per block (B <= 256), hidden sizes with H % 32 == 0 and
-// 4U x H x 2 bytes of forward weights within the LDS budget.
+// 32 sequences per block (B <= 256), hidden sizes with H % 64 == 0, the
+// forward weight slice within the register budget and the backward one
+// within the LDS budget.
 struct XShape {
   int MT, KS, U, NT, TPW, NTU, KPW;
   bool ok;
@@ -444,7 +508,7 @@ struct XShape {
 XShape xshape(int H, int B) {
   XShape x{};
   x.ok = false;
-  if (H % 32 != 0 || B > 256 || B < 1) return x;
+  if (H % 64 != 0 || B > 256 || B < 1) return x;
   x.MT = B > 128 ? 2 : 1;
   x.KS = H / 32;
   x.U = xcd_units(H);
@@ -453,9 +517,9 @@ XShape xshape(int H, int B) {
   x.TPW = (x.MT * x.NT + 3) / 4;
   x.NTU = (x.U + 15) / 16;
   x.KPW = (4 * H / 32 + 3) / 4;
-  const int64_t wf = (int64_t)x.NT * x.KS * 64 * 16;
   const int64_t wb = (int64_t)(4 * H / 32) * 4 * x.U * 16;
-  x.ok = wf <= FWD_LDS_W && wb <= BWD_LDS_W && x.TPW <= 3 && x.NTU <= 2;
+  // forward: TPW x KS/2 resident weight fragments per wave (4 VGPRs each)
+  x.ok = x.TPW * x.KS / 2 <= 36 && wb <= BWD_LDS_W && x.TPW <= 3 && x.NTU <= 2;
   return x;
 }
 
@@ -463,7 +527,7 @@ XShape xshape(int H, int B) {
 
 #define AM_FWD_CASE(MT_, KS_, TPW_)                                                      \
   if (x.MT == MT_ && x.KS == KS_ && x.TPW == TPW_)                                       \
-    return coop(lstm_fwd_xcd<bf16_t, MT_, KS_, TPW_>, blocks, lds, args, s, used);
+    return coop(lstm_fwd_xcd<MT_, KS_, TPW_>, blocks, 512, lds, args, s, used);
 
 hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used) {
   *used = false;
@@ -471,7 +535,7 @@ hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipS
   if (!x.ok) return hipSuccess;
   y.units = x.U;
   const int blocks = NX * (a.hidden / x.U);
-  const size_t lds = FWD_LDS_W + 4 * x.TPW * 64 * 16;
+  const size_t lds = (size_t)16 * x.MT * x.KS * 64 + 2 * 8 * x.TPW * 64 * 16;
   void* args[] = {&a, &ps, &y};
   // instantiated shapes: H = 768 (B <= 128 and <= 256), H = 64, 128
   AM_FWD_CASE(2, 24, 3) AM_FWD_CASE(1, 24, 2)
@@ -482,7 +546,7 @@ hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipS
 
 #define AM_BWD_CASE(MT_, NTU_, KPW_)                                                     \
   if (x.MT == MT_ && x.NTU == NTU_ && x.KPW == KPW_)                                     \
-    return coop(lstm_bwd_xcd<bf16_t, MT_, NTU_, KPW_>, blocks, lds, args, s, used);
+    return coop(lstm_bwd_xcd<bf16_t, MT_, NTU_, KPW_>, blocks, 256, lds, args, s, used);
 
 hipError_t lstm_bwd_xcd_launch(PersistBwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used) {
   *used = false;
