@@ -91,6 +91,7 @@ struct PersistFwd {
 };
 struct PersistBwd {
   const void* Wh;      // [4H][H]
+  const void* WhT;     // [H][4H] (the XCD-local kernel reads this layout)
   const void* dHa;     // [N][H] gradient from the layer above
   const void* G;       // [N][4H]
   const float* C;      // [N][H]

@@ -612,6 +612,7 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
     if (sc.N > 0 && persistent_enabled()) {
       am::PersistBwd pa;
       pa.Wh = P8 + po.wh[l] * e;
+      pa.WhT = WhT;
       pa.dHa = DH;
       pa.G = Gl;
       pa.C = Cl;
@@ -624,6 +625,10 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
       const double flops = 2.0 * (sc.N - sc.counts[0]) * G * H;
       const double bytes = (double)sc.N * (G * e * 2 + H * (e + 8)) + (double)G * H * e;
       if (bf && xcd_enabled() && am::lstm_xcd_instantiated(false, (int)H, B)) {
+        {
+          Timed tm(AM_K_MISC, s, 0.0, 2.0 * G * H * e);
+          AM_TRY(hip_check(am::transpose(P8 + po.wh[l] * e, WhT, (int)G, (int)H, bf, s), "Wh transpose"));
+        }
         AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
         Timed tm(AM_K_LSTM_BWD, s, flops, bytes);
         AM_TRY(hip_check(am::lstm_bwd_xcd_launch(pa, ps, xcd_sync(at<void>(ws, w.sync)), s, &used),

@@ -21,7 +21,8 @@
 // W_h resident in registers in unit-major, gate-minor order, so a 16-column
 // MFMA tile holds 4 units x 4 gates; a per-wave transpose of 4x4 quads
 // through LDS then gives each lane all four gate pre-activations of one
-// (sequence, unit).  The backward product keeps the U rows of W_h^T in LDS.
+// (sequence, unit).  The backward product keeps the U columns of W_h in
+// registers too.
 #include "am_device.h"
 #include "am_internal.h"
 
@@ -30,7 +31,6 @@ namespace {
 
 constexpr int NX = 8;                    // XCDs
 constexpr unsigned SPIN_LIMIT = 1u << 22;
-constexpr int BWD_LDS_W = 147456;        // bytes of resident weights, backward
 
 __device__ __forceinline__ unsigned xcc_id() {
   unsigned v;
@@ -308,49 +308,56 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
 
 // ---------------------------------------------------------------- backward --
 // dh_rec[rows][units] = dA_{t+1}[rows][4H] W_h[4H][units]: output tiles of
-// 16 units (the last one partly empty), k-range split over the 4 waves.
-// MT: row tiles; NTU: unit tiles; KPW: k-steps per wave (4H = 128 KPW).
-template <typename T, int MT, int NTU, int KPW>
-__global__ __launch_bounds__(256, 1) void lstm_bwd_xcd(PersistBwd a, PersistSchedule ps, XcdSync y) {
+// 16 units (the last one partly empty).  Eight waves split the 4H-long k
+// range: wave w multiplies k-steps [w KW, (w+1) KW) and keeps the W_h^T
+// fragments of those k-steps, for every unit tile, in registers.  Each wave
+// fetches its k-slice of the block's dA_{t+1} rows itself, with direct loads
+// into two private LDS buffers in chunks of CH k-steps, so it waits only on
+// its own loads.  The eight partial products are summed in a fixed order
+// through LDS, and waves f < MT NTU finish tile (row tile f % MT, unit tile
+// f / MT): the cell backward, with dc carried in registers.
+template <int MT, int NTU, int KW>
+__global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSchedule ps, XcdSync y) {
+  constexpr int RB = 16 * MT;                 // sequences per block
+  constexpr int CH = KW >= 4 ? 4 : KW;        // k-steps per chunk
+  constexpr int NCH = KW / CH;                // chunks per step
+  constexpr int CPR = CH * 4;                 // 16-byte pieces per chunk row
+  constexpr int SW = (CPR < 8 ? CPR : 8) - 1; // swizzle mask
+  constexpr int CHB = RB * CH * 64;           // bytes per chunk
+  constexpr int IPC = CHB / 1024;             // direct loads per chunk
+  static_assert(KW % CH == 0 && IPC >= 1, "chunking");
   extern __shared__ __align__(16) unsigned char lds[];
-  Frag<T>* wl = reinterpret_cast<Frag<T>*>(lds);                  // [n][ks][lane]
-  f32x4_t* red = reinterpret_cast<f32x4_t*>(lds + BWD_LDS_W);      // [wave][m][lane] per unit tile
+  bf16_t* buf = reinterpret_cast<bf16_t*>(lds + (threadIdx.x >> 6) * 2 * CHB);
+  f32x4_t* red = reinterpret_cast<f32x4_t*>(lds);  // [8][MT][NTU][64], after the products
   __shared__ int bad_sh;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int H = a.hidden, G4 = 4 * H, U = y.units;
-  const int ksteps = G4 / 32;
   const int blk = blockIdx.x % NX, us = blockIdx.x / NX;
-  const int b0 = blk * 16 * MT, j0 = us * U;
+  const int b0 = blk * RB, j0 = us * U;
   const int members = H / U;
-  const int koct = (lane >> 4) * 8;
-  const T* __restrict__ Wh = static_cast<const T*>(a.Wh);
-  const T* __restrict__ dHa = static_cast<const T*>(a.dHa);
-  const T* __restrict__ Gb = static_cast<const T*>(a.G);
-  T* __restrict__ dA = static_cast<T*>(a.dA);
+  const bf16_t* __restrict__ WhT = static_cast<const bf16_t*>(a.WhT);
+  const bf16_t* __restrict__ dHa = static_cast<const bf16_t*>(a.dHa);
+  const bf16_t* __restrict__ Gb = static_cast<const bf16_t*>(a.G);
+  bf16_t* __restrict__ dA = static_cast<bf16_t*>(a.dA);
 
-  // W_h^T fragments of unit tile n (vc_n = min(16, U - 16n) valid columns),
-  // k-step ks: W_h[k .. k+7][j0 + 16n + c] for c < vc_n, stored compactly at
-  // base(n) + ks * 4 vc_n + (k-octet) vc_n + c with base(n) = 64 ksteps n.
-  for (int n = 0; n < NTU; ++n) {
-    const int vc = min(16, U - 16 * n);
-    for (int e = threadIdx.x; e < ksteps * 4 * vc; e += 256) {
-      const int c = e % vc, oct = (e / vc) & 3, ks = e / (4 * vc);
-      const int k = ks * 32 + oct * 8;
-      T v[8];
+  // resident W_h^T fragments (8 consecutive k of one unit: one 16-byte load
+  // of the transposed W_h): k-step wave KW + s, unit tile n, lane column
+  // c -> unit j0 + 16n + min(c, vc_n - 1) (vc_n = valid columns of tile n)
+  Frag<bf16_t> wb[KW][NTU];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) v[q] = Wh[(int64_t)(k + q) * H + j0 + 16 * n + c];
-      Frag<T> f;
-      memcpy(&f, v, sizeof f);
-      wl[64 * ksteps * n + e] = f;
-    }
+  for (int n = 0; n < NTU; ++n) {
+    const int unit = j0 + 16 * n + min(lane & 15, min(16, U - 16 * n) - 1);
+#pragma unroll
+    for (int s = 0; s < KW; ++s)
+      wb[s][n] = frag_load<bf16_t>(WhT + (int64_t)unit * G4 + (wave * KW + s) * 32 + (lane >> 4) * 8);
   }
   const bool local = check_local(y, &bad_sh);
 
-  // finishing tile of this wave: row tile wave % MT, unit tile wave / MT
+  // finishing tile of this wave (waves f < MT NTU)
   const int fm = wave % MT, fn = wave / MT;
-  const bool fin = fn < NTU;
-  const int uu = 16 * fn + (lane & 15);              // unit within the slice
+  const bool fin = wave < MT * NTU;
+  const int uu = 16 * (fin ? fn : 0) + (lane & 15);  // unit within the slice
   const bool uok = fin && uu < U;
   const int j = j0 + (uok ? uu : 0);
   float dc_reg[4] = {0.f, 0.f, 0.f, 0.f};
@@ -370,19 +377,22 @@ __global__ __launch_bounds__(256, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
     const int nb_prev = t > 0 ? active_up(ps, nb, t - 1) : 0;
     const int off_prev = off - nb_prev;
 
-    T gv[4][4], dhv[4];
+    // the finishing waves' cell inputs (independent of the exchange)
+    bf16_t gv[4][4], dhv[4];
     float cv[4], cpv[4];
-    const float* cprev_rows = t > 0 ? a.C + (int64_t)off_prev * H : a.c0;
+    if (fin) {
+      const float* cprev_rows = t > 0 ? a.C + (int64_t)off_prev * H : a.c0;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int b = min(b0 + fm * 16 + mfma_row(lane, r), nb - 1);
-      const int64_t o = (int64_t)(off + b) * H + j;
-      const T* grow = Gb + (int64_t)(off + b) * G4;
+      for (int r = 0; r < 4; ++r) {
+        const int b = min(b0 + fm * 16 + mfma_row(lane, r), nb - 1);
+        const int64_t o = (int64_t)(off + b) * H + j;
+        const bf16_t* grow = Gb + (int64_t)(off + b) * G4;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) gv[r][g] = grow[g * H + j];
-      cv[r] = a.C[o];
-      cpv[r] = cprev_rows[(int64_t)b * H + j];
-      dhv[r] = dHa[o];
+        for (int q = 0; q < 4; ++q) gv[r][q] = grow[q * H + j];
+        cv[r] = a.C[o];
+        cpv[r] = cprev_rows[(int64_t)b * H + j];
+        dhv[r] = dHa[o];
+      }
     }
 
     f32x4_t acc[MT][NTU];
@@ -392,53 +402,55 @@ __global__ __launch_bounds__(256, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
       for (int n = 0; n < NTU; ++n) acc[m][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (b0 < nb_next) {
       xwait(y, local, (unsigned)members * done);
-      const T* dAn = dA + (int64_t)off_next * G4;
-      const T* arow[MT];
+      const bf16_t* dAn = dA + (int64_t)off_next * G4 + wave * KW * 32;
+      // chunk c of this wave's k-slice into buffer bi: RB rows x CH k-steps;
+      // instruction i covers rows i*(64/CPR) .., 16-byte pieces swizzled by row
+      auto issue = [&](int c, int bi) {
 #pragma unroll
-      for (int m = 0; m < MT; ++m)
-        arow[m] = dAn + (int64_t)min(b0 + m * 16 + (lane & 15), nb_next - 1) * G4 + koct;
-      constexpr int PH = (MT * KPW > 24) ? (24 / MT) : KPW;  // k-steps per batch of loads
+        for (int i = 0; i < IPC; ++i) {
+          const int row = i * (64 / CPR) + lane / CPR;
+          const int piece = (lane % CPR) ^ (row & SW);
+          dma16(dAn + (int64_t)min(b0 + row, nb_next - 1) * G4 + c * CH * 32 + piece * 8,
+                __builtin_amdgcn_readfirstlane(lds_address(buf + bi * (CHB / 2) + i * 512)));
+        }
+      };
+      issue(0, 0);
+      if (NCH > 1) issue(1, 1);
 #pragma unroll
-      for (int s0 = 0; s0 < KPW; s0 += PH) {
-        Frag<T> af[PH][MT];
+      for (int c = 0; c < NCH; ++c) {
+        if (c + 1 < NCH) wait_vm<IPC>();
+        else wait_vm<0>();
+        const bf16_t* bb = buf + (c & 1) * (CHB / 2);
 #pragma unroll
-        for (int s = 0; s < PH; ++s)
+        for (int ks = 0; ks < CH; ++ks) {
+          Frag<bf16_t> af[MT];
 #pragma unroll
           for (int m = 0; m < MT; ++m) {
-            const int ks = wave + 4 * (s0 + s);
-            af[s][m] = frag_load<T>(arow[m] + (s0 + s < KPW && ks < ksteps ? ks * 32 : 0));
+            const int row = m * 16 + (lane & 15), piece = ks * 4 + (lane >> 4);
+            af[m] = *reinterpret_cast<const Frag<bf16_t>*>(bb + row * CH * 32 + ((piece ^ (row & SW)) << 3));
           }
-        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int s = 0; s < PH; ++s) {
-          const int ks = wave + 4 * (s0 + s);
-          if (s0 + s >= KPW || ks >= ksteps) break;
+          for (int n = 0; n < NTU; ++n)
 #pragma unroll
-          for (int n = 0; n < NTU; ++n) {
-            // lanes past the tile's valid columns read a valid entry; their
-            // output columns are never used
-            const int vc = min(16, U - 16 * n);
-            const Frag<T> bf =
-                wl[64 * ksteps * n + ks * 4 * vc + (lane >> 4) * vc + min(lane & 15, vc - 1)];
-#pragma unroll
-            for (int m = 0; m < MT; ++m) mma_16x16x32(acc[m][n], af[s][m], bf);
-          }
+            for (int m = 0; m < MT; ++m) mma_16x16x32(acc[m][n], af[m], wb[c * CH + ks][n]);
         }
-        __builtin_amdgcn_sched_barrier(0);
+        if (c + 2 < NCH) {
+          __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this buffer's reads are done
+          issue(c + 2, c & 1);
+        }
       }
     }
-    // fixed-order sum over the 4 waves, one unit tile at a time
+    // fixed-order sum of the eight partial products
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int n = 0; n < NTU; ++n) red[((wave * MT + m) * NTU + n) * 64 + lane] = acc[m][n];
+    __syncthreads();
     f32x4_t rec = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (fin) {
 #pragma unroll
-    for (int n = 0; n < NTU; ++n) {
-#pragma unroll
-      for (int m = 0; m < MT; ++m) red[(wave * MT + m) * 64 + lane] = acc[m][n];
-      __syncthreads();
-      if (fn == n) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) rec += red[(v * MT + fm) * 64 + lane];
-      }
-      __syncthreads();
+      for (int w = 0; w < 8; ++w) rec += red[((w * MT + fm) * NTU + fn) * 64 + lane];
     }
 
 #pragma unroll
@@ -446,21 +458,21 @@ __global__ __launch_bounds__(256, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
       const int b = b0 + fm * 16 + mfma_row(lane, r);
       if (!uok || b >= nb) continue;
       const bool cont = b < nb_next;
-      const float vi = to_f32<T>(gv[r][0]), vf = to_f32<T>(gv[r][1]);
-      const float vg = to_f32<T>(gv[r][2]), vo = to_f32<T>(gv[r][3]);
-      const float dhh = to_f32<T>(dhv[r]) + (cont ? rec[r] : 0.f);
+      const float vi = bf16_to_f32(gv[r][0]), vf = bf16_to_f32(gv[r][1]);
+      const float vg = bf16_to_f32(gv[r][2]), vo = bf16_to_f32(gv[r][3]);
+      const float dhh = bf16_to_f32(dhv[r]) + (cont ? rec[r] : 0.f);
       const float tc = tanh_f(cv[r]);
       const float d_o = dhh * tc;
       const float dcell = dhh * vo * (1.f - tc * tc) + (cont ? dc_reg[r] : 0.f);
       const float d_i = dcell * vg, d_g = dcell * vi, d_f = dcell * cpv[r];
       dc_reg[r] = dcell * vf;
-      T* arow = dA + (int64_t)(off + b) * G4;
-      arow[j] = from_f32<T>(d_i * vi * (1.f - vi));
-      arow[H + j] = from_f32<T>(d_f * vf * (1.f - vf));
-      arow[2 * H + j] = from_f32<T>(d_g * (1.f - vg * vg));
-      arow[3 * H + j] = from_f32<T>(d_o * vo * (1.f - vo));
+      bf16_t* arow = dA + (int64_t)(off + b) * G4;
+      arow[j] = f32_to_bf16(d_i * vi * (1.f - vi));
+      arow[H + j] = f32_to_bf16(d_f * vf * (1.f - vf));
+      arow[2 * H + j] = f32_to_bf16(d_g * (1.f - vg * vg));
+      arow[3 * H + j] = f32_to_bf16(d_o * vo * (1.f - vo));
     }
-    xsignal(y, local);
+    xsignal(y, local);  // its barrier also orders the LDS reuse
     ++done;
   }
 }
@@ -501,7 +513,7 @@ hipError_t coop(K kernel, int blocks, int threads, size_t lds, void** args, hipS
 // forward weight slice within the register budget and the backward one
 // within the LDS budget.
 struct XShape {
-  int MT, KS, U, NT, TPW, NTU, KPW;
+  int MT, KS, U, NT, TPW, NTU, KW;
   bool ok;
 };
 
@@ -516,10 +528,10 @@ XShape xshape(int H, int B) {
   x.NT = x.U / 4;
   x.TPW = (x.MT * x.NT + 3) / 4;
   x.NTU = (x.U + 15) / 16;
-  x.KPW = (4 * H / 32 + 3) / 4;
-  const int64_t wb = (int64_t)(4 * H / 32) * 4 * x.U * 16;
-  // forward: TPW x KS/2 resident weight fragments per wave (4 VGPRs each)
-  x.ok = x.TPW * x.KS / 2 <= 36 && wb <= BWD_LDS_W && x.TPW <= 3 && x.NTU <= 2;
+  x.KW = 4 * H / 32 / 8;  // backward k-steps per wave (eight waves)
+  // resident weight fragments per wave (4 VGPRs each): forward TPW x KS/2,
+  // backward KW x NTU
+  x.ok = x.TPW * x.KS / 2 <= 36 && x.KW * x.NTU <= 24 && x.TPW <= 3 && x.NTU <= 2;
   return x;
 }
 
@@ -544,9 +556,9 @@ hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipS
   return hipSuccess;
 }
 
-#define AM_BWD_CASE(MT_, NTU_, KPW_)                                                     \
-  if (x.MT == MT_ && x.NTU == NTU_ && x.KPW == KPW_)                                     \
-    return coop(lstm_bwd_xcd<bf16_t, MT_, NTU_, KPW_>, blocks, 256, lds, args, s, used);
+#define AM_BWD_CASE(MT_, NTU_, KW_)                                                       \
+  if (x.MT == MT_ && x.NTU == NTU_ && x.KW == KW_)                                       \
+    return coop(lstm_bwd_xcd<MT_, NTU_, KW_>, blocks, 512, lds, args, s, used);
 
 hipError_t lstm_bwd_xcd_launch(PersistBwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used) {
   *used = false;
@@ -554,11 +566,15 @@ hipError_t lstm_bwd_xcd_launch(PersistBwd a, PersistSchedule ps, XcdSync y, hipS
   if (!x.ok) return hipSuccess;
   y.units = x.U;
   const int blocks = NX * (a.hidden / x.U);
-  const size_t lds = BWD_LDS_W + 4 * x.MT * 64 * 16;
+  // two private chunk buffers per wave, or the partial products if larger
+  const int ch = x.KW >= 4 ? 4 : x.KW;
+  const size_t chunks = (size_t)8 * 2 * 16 * x.MT * ch * 64;
+  const size_t red = (size_t)8 * x.MT * x.NTU * 64 * 16;
+  const size_t lds = chunks > red ? chunks : red;
   void* args[] = {&a, &ps, &y};
-  AM_BWD_CASE(2, 2, 24) AM_BWD_CASE(1, 2, 24)
+  AM_BWD_CASE(2, 2, 12) AM_BWD_CASE(1, 2, 12)
+  AM_BWD_CASE(2, 1, 1) AM_BWD_CASE(1, 1, 1)
   AM_BWD_CASE(2, 1, 2) AM_BWD_CASE(1, 1, 2)
-  AM_BWD_CASE(2, 1, 4) AM_BWD_CASE(1, 1, 4)
   return hipSuccess;
 }
 
@@ -568,7 +584,7 @@ bool lstm_xcd_instantiated(bool forward, int hidden, int B) {
   if (forward)
     return (x.KS == 24 && ((x.MT == 2 && x.TPW == 3) || (x.MT == 1 && x.TPW == 2))) ||
            ((x.KS == 2 || x.KS == 4) && x.TPW == 1);
-  return (x.KPW == 24 && x.NTU == 2) || ((x.KPW == 2 || x.KPW == 4) && x.NTU == 1);
+  return (x.KW == 12 && x.NTU == 2) || ((x.KW == 1 || x.KW == 2) && x.NTU == 1);
 }
 
 }  // namespace am
