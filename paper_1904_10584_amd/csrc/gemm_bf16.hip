@@ -3,46 +3,85 @@
 //   data gradients       dH = dZ Wo,  dX = dA Wx              (B n-major)
 //   weight gradients     [dWx | dWh] = dA^T [X | Hs],  dWo = dZ^T H
 //                                                  (A m-major, B n-major)
-// Each operand tile is copied to LDS in its global layout with 16-byte
-// loads and stores; no operand is transposed in registers:
+// Design, from measurements on MI355X:
+//   * operand tiles go from global memory straight to LDS (global_load_lds,
+//     16 bytes per lane), which moves about 2.5x the bytes per CU per clock
+//     of loads into VGPRs; fed through VGPRs, a GEMM tops out near a
+//     quarter of the MFMA peak;
+//   * one wave per SIMD issues MFMAs at half the rate two waves do, so a
+//     workgroup is eight waves (two per SIMD, one workgroup per CU);
+//   * a 256 x BN tile (BN = 256, or 192 where that fills the CUs) with waves
+//     of 128 x BN/4 reads 384 bytes or less of LDS per MFMA.
+// Tiles keep their global layout in LDS:
 //   * a k-major tile is [rows][64 k] (128 B per row); the fragment of a
 //     16x16x32 MFMA (8 consecutive k of one row per lane) is one 16-byte LDS
 //     read;
 //   * an m/n-major tile is [64 k][rows]; the fragment is read with two
-//     gfx950 transposing LDS reads (ds_read_b64_tr_b16).  Within each group
-//     of 16 lanes, lane i receives element i % 4 of the 4-element pieces
-//     addressed by lanes 4q + i / 4 (q = 0..3); so when lane j of the group
-//     addresses k-row k0 + j / 4 at column c0 + 4 (j % 4), lane i receives
-//     column c0 + i at k-rows k0 .. k0 + 3.
-// Both layouts XOR-swizzle their 16-byte chunks so that the fragment reads
-// and the tile stores are free of LDS bank conflicts.
-// One 256-thread workgroup computes a 128x128 tile (four waves of 64x64 as
-// 4x4 MFMA tiles); the global loads of k-tile t+2 are in flight while tile t
-// is multiplied (two register stages, two LDS stages).
-// Workgroups are dispatched to the 8 XCDs round-robin; the tile order gives
-// each XCD a contiguous range of tiles, so tiles that share operand rows
-// share an L2.
-// Weight gradients split K over workgroups (fp32 partial tiles, summed in
-// split order by splitk_reduce in gemm.hip) and, for an m-major A, also
-// produce the row sums of A over each split (the bias gradient).
+//     transposing LDS reads (ds_read_b64_tr_b16).  Within each group of 16
+//     lanes, lane i receives element i % 4 of the 4-element pieces addressed
+//     by lanes 4q + i / 4 (q = 0..3); so when lane j of the group addresses
+//     k-row k0 + j / 4 at column c0 + 4 (j % 4), lane i receives column
+//     c0 + i at k-rows k0 .. k0 + 3.
+// Both layouts XOR-swizzle their 16-byte chunks (the direct-load lane that
+// fills a slot fetches the chunk that belongs there), which makes the
+// fragment reads free of LDS bank conflicts and keeps each 128-byte line of
+// a tile row in one load instruction.  Chunks outside the operand are read
+// from a zero vector.  The loads of k-tile t + NS - 1 are in flight while
+// tile t is multiplied (NS LDS stages, explicit vmcnt waits, one barrier per
+// k-tile).  Workgroups are dispatched to the 8 XCDs round-robin; the tile
+// order gives each XCD a contiguous range of tiles, so tiles that share
+// operand rows share an L2.  Weight gradients split K over workgroups (fp32
+// partial tiles, summed in split order by splitk_reduce in gemm.hip); for an
+// m-major A the first column of tiles also forms the row sums of A (the bias
+// gradient) with one more MFMA per row tile against a fragment of ones.
 #include "am_device.h"
 #include "am_internal.h"
 
 namespace am {
 namespace {
 
-constexpr int TB = 128;   // tile rows and columns
 constexpr int BK = 64;    // k per tile
-constexpr int NT = 256;   // threads per workgroup
+constexpr int BM = 256;   // tile rows
+constexpr int NT = 512;   // threads per workgroup (8 waves: 2 x 4)
+constexpr int NW = 8;
 constexpr int NX = 8;     // XCDs
+
+__device__ uint4 g_zero[1];  // 16 zero bytes (the source of out-of-range chunks)
+
+template <int BN> struct Cfg {
+  static constexpr int WM = BM / 2;            // wave tile rows
+  static constexpr int WN = BN / 4;            // wave tile columns
+  static constexpr int MI = WM / 16;           // 8
+  static constexpr int NJ = WN / 16;           // 4 or 3
+  static constexpr int A_BYTES = BM * BK * 2;
+  static constexpr int B_BYTES = BN * BK * 2;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int NS = 3 * STAGE <= 150 * 1024 ? 3 : 2;  // LDS stages
+  static constexpr int LDS = NS * STAGE;
+  static constexpr int A_IPW = A_BYTES / 1024 / NW;  // direct loads per wave per tile
+  static constexpr int B_IPW = B_BYTES / 1024 / NW;
+  static constexpr int IPW = A_IPW + B_IPW;
+  static_assert(A_BYTES % (1024 * NW) == 0 && B_BYTES % (1024 * NW) == 0, "tile split");
+};
 
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
 
 // Element offset of chunk c (8 bf16) of row r in a k-major tile.
 __device__ __forceinline__ int kofs(int r, int c) { return r * BK + ((c ^ (r & 7)) << 3); }
-// Element offset of chunk c of k-row k in an m/n-major tile of TB columns.
-__device__ __forceinline__ int mofs(int k, int c) { return k * TB + ((c ^ ((k & 3) << 1)) << 3); }
+// Element offset of chunk c of k-row k in an m/n-major tile of R columns.
+template <int R> __device__ __forceinline__ int mofs(int k, int c) {
+  return k * R + ((c ^ ((k & 3) << 1)) << 3);
+}
+
+// Workgroup barrier without a memory fence (a fence would wait for every
+// load in flight, including the later tiles' direct loads).  The empty asm
+// statements keep the compiler from moving memory accesses across it.
+__device__ __forceinline__ void tile_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 // One operand: rows (of the tile dimension) below `split` come from p0, the
 // others from p1 at row - split.
@@ -52,50 +91,41 @@ struct Op {
   int split;
 };
 
-// Global -> register stage of one operand tile: 4 chunks per thread.
-template <bool KMAJOR, bool SUM> struct Stage {
-  uint4 v[4];
-  __device__ __forceinline__ void load(const Op& o, int row0, int nrows, int k0, int kend) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int idx = threadIdx.x + NT * j;
-      int r, k;
-      if (KMAJOR) { r = idx >> 3; k = k0 + ((idx & 7) << 3); }
-      else { r = (idx & 15) << 3; k = k0 + (idx >> 4); }
-      const int gr = row0 + r;
-      const bool sec = gr >= o.split;
-      const bf16_t* p = sec ? o.p1 : o.p0;
-      const int64_t ld = sec ? o.ld1 : o.ld0;
-      const int rr = sec ? gr - o.split : gr;
-      const bool ok = gr < nrows && k < kend;
-      const int64_t off = KMAJOR ? (int64_t)rr * ld + k : (int64_t)k * ld + rr;
-      v[j] = ok ? *reinterpret_cast<const uint4*>(p + off) : make_uint4(0, 0, 0, 0);
-    }
-  }
-  __device__ __forceinline__ void store(bf16_t* lds) const {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int idx = threadIdx.x + NT * j;
-      const int o = KMAJOR ? kofs(idx >> 3, idx & 7) : mofs(idx >> 4, idx & 15);
-      *reinterpret_cast<uint4*>(lds + o) = v[j];
-    }
-  }
-  // m-major only: this thread's 8 rows summed over its 4 k-rows of the tile.
-  __device__ __forceinline__ void accumulate(float* rs) const {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        rs[2 * e] += __uint_as_float(w[e] << 16);
-        rs[2 * e + 1] += __uint_as_float(w[e] & 0xFFFF0000u);
-      }
-    }
-  }
-};
+__device__ __forceinline__ const bf16_t* op_ptr(const Op& o, int row, int k, bool kmajor) {
+  const bool sec = row >= o.split;
+  const bf16_t* p = sec ? o.p1 : o.p0;
+  const int64_t ld = sec ? o.ld1 : o.ld0;
+  const int r = sec ? row - o.split : row;
+  return kmajor ? p + (int64_t)r * ld + k : p + (int64_t)k * ld + r;
+}
 
-// Fragment of rows/columns r0 .. r0+15, k-step ks of the tile.
-template <bool KMAJOR>
+// Issue direct load j of this wave for one R-row operand tile (R * BK * 2
+// bytes in R / 8 loads of 1 KiB, R / 8 / NW per wave).
+template <bool KMAJOR, int R>
+__device__ __forceinline__ void dma_one(const Op& o, int row0, int nrows, int k0, int kend,
+                                        const bf16_t* lds, int wave, int lane, int j) {
+  {
+    const int q = wave + NW * j;
+    int row, k;
+    if (KMAJOR) {  // 8 rows x 8 chunks per load
+      const int r = 8 * q + (lane >> 3);
+      row = row0 + r;
+      k = k0 + (((lane & 7) ^ (r & 7)) << 3);
+    } else {       // k-rows of R / 8 chunks, laid end to end
+      constexpr int CPR = R / 8;
+      const int e = q * 64 + lane;  // chunk index in the tile
+      const int kr = e / CPR;
+      k = k0 + kr;
+      row = row0 + (((e % CPR) ^ ((kr & 3) << 1)) << 3);
+    }
+    const bool ok = row < nrows && k < kend;
+    const void* src = ok ? (const void*)op_ptr(o, row, k, KMAJOR) : (const void*)g_zero;
+    dma16(src, __builtin_amdgcn_readfirstlane(lds_address(lds + q * 512)));
+  }
+}
+
+// Fragment of rows/columns r0 .. r0+15, k-step ks of an R-row tile.
+template <bool KMAJOR, int R>
 __device__ __forceinline__ Frag<bf16_t> frag(const bf16_t* lds, int r0, int ks, int lane) {
   Frag<bf16_t> f;
   if (KMAJOR) {
@@ -104,11 +134,11 @@ __device__ __forceinline__ Frag<bf16_t> frag(const bf16_t* lds, int r0, int ks, 
     const int j = lane & 15;
     const int k = ks * 32 + (lane >> 4) * 8 + (j >> 2);
     const int col = r0 + ((j & 3) << 2);
-    const int c = col >> 3, half = (col & 7);
+    const int c = col >> 3, half = col & 7;
     const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_v4s_t*)(lds + mofs(k, c) + half));
+        (lds_v4s_t*)(lds + mofs<R>(k, c) + half));
     const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_v4s_t*)(lds + mofs(k + 4, c) + half));
+        (lds_v4s_t*)(lds + mofs<R>(k + 4, c) + half));
     f.v = make_uint4((uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16),
                      (uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16),
                      (uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16),
@@ -126,100 +156,95 @@ template <typename OutT> struct Out {
 
 // ROWSUM: A is m-major; the workgroups of the first column of tiles write
 // the row sums of A over their split's k-range to rowsum[z * M + m].
-template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM>
-__global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(
+template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN>
+__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
     Op A, Op B, Out<OutT> C, const bf16_t* __restrict__ bias, float* __restrict__ rowsum,
     int M, int N, int K, int kps, int tm, int tn, int S) {
-  __shared__ __align__(16) bf16_t smem[2][2][TB * BK];  // [stage][A|B]
+  using CF = Cfg<BN>;
+  extern __shared__ __align__(16) bf16_t smem[];
 
   // XCD-contiguous tile order: workgroup b runs on XCD b % 8.
   const int G = tm * tn * S;
   const int b = blockIdx.x, x = b % NX, q = G / NX, rem = G % NX;
   const int T = x * q + min(x, rem) + b / NX;
   const int z = T / (tm * tn), t2 = T % (tm * tn);
-  const int m0 = (t2 / tn) * TB, n0 = (t2 % tn) * TB;
+  const int m0 = (t2 / tn) * BM, n0 = (t2 % tn) * BN;
   const int kbeg = z * kps, kend = min(K, kbeg + kps);
-  const bool do_sum = ROWSUM && n0 == 0;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+  const int wm = (wave >> 2) * CF::WM, wn = (wave & 3) * CF::WN;
+  const bool do_sum = ROWSUM && n0 == 0 && (wave & 3) == 0;
 
-  f32x4_t acc[4][4];
+  f32x4_t acc[CF::MI][CF::NJ];
+  f32x4_t accs[ROWSUM ? CF::MI : 1];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < CF::MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float rs[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < CF::NJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < (ROWSUM ? CF::MI : 1); ++i) accs[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  Frag<bf16_t> ones;
+  ones.v = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
 
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
-  Stage<AK, ROWSUM> sa[2];
-  Stage<BKM, false> sb[2];
-  if (nk > 0) {
-    sa[0].load(A, m0, M, kbeg, kend);
-    sb[0].load(B, n0, N, kbeg, kend);
-  }
-  if (nk > 1) {
-    sa[1].load(A, m0, M, kbeg + BK, kend);
-    sb[1].load(B, n0, N, kbeg + BK, kend);
-  }
-  if (nk > 0) {
-    if (do_sum) sa[0].accumulate(rs);
-    sa[0].store(smem[0][0]);
-    sb[0].store(smem[0][1]);
-  }
-  __syncthreads();
+  // direct load `idx` (< IPW) of this wave for k-tile t
+  auto dma = [&](int t, int idx) {
+    const bf16_t* st = smem + (t % CF::NS) * (CF::STAGE / 2);
+    if (idx < CF::A_IPW) dma_one<AK, BM>(A, m0, M, kbeg + t * BK, kend, st, wave, lane, idx);
+    else dma_one<BKM, BN>(B, n0, N, kbeg + t * BK, kend, st + CF::A_BYTES / 2, wave, lane,
+                          idx - CF::A_IPW);
+  };
+#pragma unroll
+  for (int p = 0; p < CF::NS - 1; ++p)
+    if (p < nk) {
+#pragma unroll
+      for (int idx = 0; idx < CF::IPW; ++idx) dma(p, idx);
+    }
 
-  // Two k-tiles per pass so that the register stages are indexed statically.
-  for (int kt = 0; kt < nk; kt += 2) {
+  for (int t = 0; t < nk; ++t) {
+    // this wave's loads of tile t are done once at most the later tiles'
+    // loads are outstanding; the barrier makes that true for every wave and
+    // retires every read of the stage the next loads overwrite
+    if (nk - 1 - t >= CF::NS - 2) wait_vm<(CF::NS - 2) * CF::IPW>();
+    else wait_vm<0>();
+    tile_barrier();
+    // the next tile's direct loads are spread through this tile's MFMAs (one
+    // after each row tile), so that the memory pipeline works while the
+    // matrix core does, instead of every wave queueing its loads at once
+    const bool more = t + CF::NS - 1 < nk;
+
+    const bf16_t* la = smem + (t % CF::NS) * (CF::STAGE / 2);
+    const bf16_t* lb = la + CF::A_BYTES / 2;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int t = kt + u;
-      if (t >= nk) break;
-      // stage u is free (stored at the previous tile): fetch tile t + 2
-      if (t + 2 < nk) {
-        sa[u].load(A, m0, M, kbeg + (t + 2) * BK, kend);
-        sb[u].load(B, n0, N, kbeg + (t + 2) * BK, kend);
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      Frag<bf16_t> af[CF::MI], bfr[CF::NJ];
+#pragma unroll
+      for (int j = 0; j < CF::NJ; ++j) bfr[j] = frag<BKM, BN>(lb, wn + 16 * j, ks, lane);
+#pragma unroll
+      for (int i = 0; i < CF::MI; ++i) af[i] = frag<AK, BM>(la, wm + 16 * i, ks, lane);
+#pragma unroll
+      for (int i = 0; i < CF::MI; ++i) {
+#pragma unroll
+        for (int j = 0; j < CF::NJ; ++j) mma_16x16x32(acc[i][j], af[i], bfr[j]);
+        if (do_sum) mma_16x16x32(accs[ROWSUM ? i : 0], af[i], ones);
+        const int idx = ks * CF::MI + i;
+        if (idx < CF::IPW && more) dma(t + CF::NS - 1, idx);
       }
-      const bf16_t* la = smem[u][0];
-      const bf16_t* lb = smem[u][1];
-#pragma unroll
-      for (int ks = 0; ks < BK / 32; ++ks) {
-        Frag<bf16_t> af[4], bf[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) af[i] = frag<AK>(la, wm + 16 * i, ks, lane);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) bf[j] = frag<BKM>(lb, wn + 16 * j, ks, lane);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) mma_16x16x32(acc[i][j], af[i], bf[j]);
-      }
-      // tile t + 1 (register stage 1 - u) goes to LDS stage 1 - u
-      if (t + 1 < nk) {
-        if (do_sum) sa[1 - u].accumulate(rs);
-        sa[1 - u].store(smem[1 - u][0]);
-        sb[1 - u].store(smem[1 - u][1]);
-      }
-      __syncthreads();
     }
   }
 
-  if (do_sum) {  // LDS is free after the loop's final barrier
-    float* red = reinterpret_cast<float*>(&smem[0][0][0]);  // [16][TB]
-    const int c = threadIdx.x & 15, kr = threadIdx.x >> 4;
+  if (do_sum && mfma_col(lane) == 0) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) red[kr * TB + c * 8 + e] = rs[e];
-    __syncthreads();
-    if (threadIdx.x < TB && m0 + (int)threadIdx.x < M) {
-      float s = 0.f;
+    for (int i = 0; i < CF::MI; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s += red[r * TB + threadIdx.x];
-      rowsum[(int64_t)z * M + m0 + threadIdx.x] = s;
-    }
+      for (int r = 0; r < 4; ++r) {
+        const int row = m0 + wm + i * 16 + mfma_row(lane, r);
+        if (row < M) rowsum[(int64_t)z * M + row] = accs[ROWSUM ? i : 0][r];
+      }
   }
 
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < CF::NJ; ++j) {
     const int col = n0 + wn + j * 16 + mfma_col(lane);
     if (col >= N) continue;
     const float bv = BIAS ? bf16_to_f32(bias[col]) : 0.f;
@@ -228,7 +253,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(
     const int64_t ldc = sec ? C.ld1 : C.ld0;
     const int cc = sec ? col - C.split : col;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < CF::MI; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = m0 + wm + i * 16 + mfma_row(lane, r);
@@ -237,17 +262,26 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(
   }
 }
 
-template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM>
-void launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kps, hipStream_t s) {
+template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN>
+hipError_t launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kps, hipStream_t s) {
+  auto kern = gemm_bf16_kernel<AK, BKM, OutT, BIAS, ROWSUM, BN>;
+  static bool attr = false;  // per instantiation
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             Cfg<BN>::LDS);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
   const bf16_t* a = static_cast<const bf16_t*>(g.A);
   const bf16_t* b = static_cast<const bf16_t*>(g.B);
   const bf16_t* b2 = g.B2 ? static_cast<const bf16_t*>(g.B2) : b;
   Op A{a, g.lda, a, g.lda, 1 << 30};
   Op B{b, g.ldb, b2, g.B2 ? g.ldb2 : g.ldb, g.B2 ? g.n_split : (1 << 30)};
-  const int tm = (g.M + TB - 1) / TB, tn = (g.N + TB - 1) / TB;
-  hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKM, OutT, BIAS, ROWSUM>), dim3(tm * tn * S), dim3(NT),
-                     0, s, A, B, dst, static_cast<const bf16_t*>(g.bias), rowsum, g.M, g.N, g.K,
-                     kps, tm, tn, S);
+  const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
+  hipLaunchKernelGGL(kern, dim3(tm * tn * S), dim3(NT), Cfg<BN>::LDS, s, A, B, dst,
+                     static_cast<const bf16_t*>(g.bias), rowsum, g.M, g.N, g.K, kps, tm, tn, S);
+  return hipGetLastError();
 }
 
 template <typename OutT> Out<OutT> direct_out(const GemmArgs& g) {
@@ -261,45 +295,88 @@ template <typename OutT> Out<OutT> direct_out(const GemmArgs& g) {
   return d;
 }
 
+int device_cus() {
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+  }
+  return cus;
+}
+
+// Relative time of a grid of w equal workgroups of `work` units each, one
+// workgroup per CU at a time.
+double grid_time(int64_t w, double work) {
+  const int cus = device_cus();
+  return (double)((w + cus - 1) / cus) * work;
+}
+
+// Tile width: 256, or 192 when its grid keeps the CUs busier.
+int pick_bn(int M, int N) {
+  const int64_t tm = (M + BM - 1) / BM;
+  const double t256 = grid_time(tm * ((N + 255) / 256), 256.0);
+  const double t192 = grid_time(tm * ((N + 191) / 192), 192.0);
+  return t192 < t256 ? 192 : 256;
+}
+
+template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM>
+hipError_t launch_bn(int bn, const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kps,
+                     hipStream_t s) {
+  return bn == 192 ? launch<AK, BKM, OutT, BIAS, ROWSUM, 192>(g, dst, rowsum, S, kps, s)
+                   : launch<AK, BKM, OutT, BIAS, ROWSUM, 256>(g, dst, rowsum, S, kps, s);
+}
+
 }  // namespace
 
 hipError_t gemm_bf16(const GemmArgs& g, hipStream_t s) {
   if (g.a_kmajor && g.b_kmajor) {  // forward projections
+    const int bn = pick_bn(g.M, g.N);
     if (g.c_f32) {
-      if (g.bias) launch<true, true, float, true, false>(g, direct_out<float>(g), nullptr, 1, g.K, s);
-      else launch<true, true, float, false, false>(g, direct_out<float>(g), nullptr, 1, g.K, s);
-    } else {
-      if (g.bias) launch<true, true, bf16_t, true, false>(g, direct_out<bf16_t>(g), nullptr, 1, g.K, s);
-      else launch<true, true, bf16_t, false, false>(g, direct_out<bf16_t>(g), nullptr, 1, g.K, s);
+      return g.bias ? launch_bn<true, true, float, true, false>(bn, g, direct_out<float>(g), nullptr, 1, g.K, s)
+                    : launch_bn<true, true, float, false, false>(bn, g, direct_out<float>(g), nullptr, 1, g.K, s);
     }
-    return hipGetLastError();
+    return g.bias ? launch_bn<true, true, bf16_t, true, false>(bn, g, direct_out<bf16_t>(g), nullptr, 1, g.K, s)
+                  : launch_bn<true, true, bf16_t, false, false>(bn, g, direct_out<bf16_t>(g), nullptr, 1, g.K, s);
   }
   if (g.a_kmajor && !g.b_kmajor && !g.bias && !g.rowsum) {  // data gradients
-    if (g.c_f32) launch<true, false, float, false, false>(g, direct_out<float>(g), nullptr, 1, g.K, s);
-    else launch<true, false, bf16_t, false, false>(g, direct_out<bf16_t>(g), nullptr, 1, g.K, s);
-    return hipGetLastError();
+    const int bn = pick_bn(g.M, g.N);
+    return g.c_f32 ? launch_bn<true, false, float, false, false>(bn, g, direct_out<float>(g), nullptr, 1, g.K, s)
+                   : launch_bn<true, false, bf16_t, false, false>(bn, g, direct_out<bf16_t>(g), nullptr, 1, g.K, s);
   }
   if (!g.a_kmajor && !g.b_kmajor && !g.bias && g.c_f32) {  // weight gradients
-    const int tiles = ((g.N + TB - 1) / TB) * ((g.M + TB - 1) / TB);
+    // (the row-sum variant keeps within the register budget at BN = 192)
+    constexpr int bn = 192;
+    const int64_t tiles = (int64_t)((g.N + bn - 1) / bn) * ((g.M + BM - 1) / BM);
     const int ktiles = (g.K + BK - 1) / BK;
+    // splits: least estimated time = rounds of one workgroup per CU over
+    // the k-range (tiles at ~60 % of the MFMA peak per CU) plus writing and
+    // re-reading the fp32 partials (~4 TB/s)
     int S = 1;
     if (g.ws) {
-      S = (512 + tiles - 1) / tiles;
-      S = S > 8 ? 8 : S;
-      while (S > 1 && ktiles / S < 8) --S;  // keep at least 8 k-tiles per split
-      while (S > 1 && (int64_t)S * g.M * g.N + (int64_t)S * g.M > g.ws_floats) --S;
+      const double t_tile = 2.0 * BM * bn * (double)g.K / (2.5e15 / device_cus() * 0.6);
+      const double t_part = (double)g.M * g.N * 8.0 / 4e12;
+      double best = 1e30;
+      for (int c = 1; c <= 8; ++c) {
+        if (c > 1 && ktiles / c < 8) break;  // at least 8 k-tiles per split
+        if (c > 1 && (int64_t)c * g.M * g.N + (int64_t)c * g.M > g.ws_floats) break;
+        const double cost = grid_time(tiles * c, t_tile / c) + (c > 1 ? c * t_part : 0.0);
+        if (cost < best) { best = cost; S = c; }
+      }
     }
     if (S == 1) {
-      if (g.rowsum) launch<false, false, float, false, true>(g, direct_out<float>(g), g.rowsum, 1, g.K, s);
-      else launch<false, false, float, false, false>(g, direct_out<float>(g), nullptr, 1, g.K, s);
-      return hipGetLastError();
+      return g.rowsum ? launch<false, false, float, false, true, bn>(g, direct_out<float>(g), g.rowsum, 1, g.K, s)
+                      : launch<false, false, float, false, false, bn>(g, direct_out<float>(g), nullptr, 1, g.K, s);
     }
     const int kps = ((ktiles + S - 1) / S) * BK;
     float* part = g.ws;
     float* rs_part = g.ws + (int64_t)S * g.M * g.N;
     Out<float> d{part, g.N, part, g.N, 1 << 30, (int64_t)g.M * g.N};  // one slice per split
-    if (g.rowsum) launch<false, false, float, false, true>(g, d, rs_part, S, kps, s);
-    else launch<false, false, float, false, false>(g, d, nullptr, S, kps, s);
+    const hipError_t e = g.rowsum ? launch<false, false, float, false, true, bn>(g, d, rs_part, S, kps, s)
+                                  : launch<false, false, float, false, false, bn>(g, d, nullptr, S, kps, s);
+    if (e != hipSuccess) return e;
     return splitk_reduce_launch(part, S, g, rs_part, s);
   }
   return hipErrorInvalidValue;
