@@ -18,8 +18,10 @@ What it computes, in the order the training step runs it
 * ``sgd``      -- the local mini-batch SGD update (§VI, §VI-B) and the
   round-to-nearest-even bf16 copy of the updated fp32 master weights.
 * ``gtc``      -- Gradient Threshold Compression (§VI-A): residual error
-  feedback, +-tau one-bit quantisation and 32-bit index/sign packing, and
-  the matching decode.
+  feedback, +-tau one-bit quantisation and 32-bit index/sign packing, the
+  matching decode, and the aggregate of several workers' sparse updates.
+* ``bmuf``     -- the BMUF-NBM global step that ends a block of local SGD
+  (§VI-B, eqs. (1)-(5)).
 
 Floating point: the model, loss and their gradients are computed in fp64;
 the quantiser and SGD use the exact fp32 operation order that the method
@@ -33,12 +35,14 @@ from .numerics import bf16_round, bf16_bits, bf16_bits_to_f32
 from .lstm_am import batch_schedule, lstm_am_forward, lstm_am_backward
 from .soft_ce import sparse_soft_ce
 from .sgd import sgd_apply
-from .gtc import grad_threshold_encode, grad_threshold_decode
+from .gtc import grad_threshold_encode, grad_threshold_decode, grad_threshold_decode_multi
+from .bmuf import bmuf_block_update, bmuf_zeta
 
 __all__ = [
     "ModelDims", "param_count", "param_offsets", "unpack_params",
     "bf16_round", "bf16_bits", "bf16_bits_to_f32",
     "batch_schedule", "lstm_am_forward", "lstm_am_backward",
     "sparse_soft_ce", "sgd_apply",
-    "grad_threshold_encode", "grad_threshold_decode",
+    "grad_threshold_encode", "grad_threshold_decode", "grad_threshold_decode_multi",
+    "bmuf_block_update", "bmuf_zeta",
 ]

@@ -60,3 +60,41 @@ def grad_threshold_decode(words, count, tau, n, dense=None, accumulate=False):
         out = np.zeros(n, dtype=np.float32)
         out[index] = value
     return out
+
+
+def grad_threshold_decode_multi(words, counts, tau, n, dense=None, accumulate=False):
+    """Aggregate of the sparse updates of several workers (§VI-A: every worker
+    receives all sparse updates and aggregates them).
+
+    words  [S][capacity] uint32, one encode output per worker
+    counts [S]: number of valid words in each row
+    The aggregate of element i is tau times the integer sum k_i of the signs
+    (+1, or -1 for sign bit 1) of all words that name i, so it does not depend
+    on the order of the workers.  Reading: it is evaluated as the exact product
+    tau * k_i rounded once to fp32.
+    accumulate=False: dense[i] = fl32(tau * k_i) where some word names i, +0.0
+    elsewhere.  accumulate=True: dense[i] = fl32(dense[i] + fl32(tau * k_i))
+    where some word names i, unchanged elsewhere.
+    """
+    tau = np.float32(tau)
+    w = np.asarray(words, dtype=np.uint32)
+    if w.ndim == 1:
+        w = w[None, :]
+    k = np.zeros(n, dtype=np.int64)
+    hit = np.zeros(n, dtype=bool)
+    for s in range(w.shape[0]):
+        ws = w[s, :int(counts[s])]
+        index = (ws >> np.uint32(1)).astype(np.int64)
+        assert np.all(index < n)
+        sign = np.where((ws & np.uint32(1)) != 0, -1, 1)
+        np.add.at(k, index, sign)
+        hit[index] = True
+    v = (np.float64(tau) * k.astype(np.float64)).astype(np.float32)
+    if accumulate:
+        out = np.array(dense, dtype=np.float32, copy=True)
+        assert out.shape == (n,)
+        out[hit] = out[hit] + v[hit]
+    else:
+        out = np.zeros(n, dtype=np.float32)
+        out[hit] = v[hit]
+    return out

@@ -151,3 +151,85 @@ def test_decode_modes_and_word_format():
     # the word packs a 31-bit index and the sign in bit 0
     w = struct.unpack("<I", struct.pack("<I", (12345 << 1) | 1))[0]
     assert (w >> 1, w & 1) == (12345, 1)
+
+
+# ---- aggregate of several workers' sparse updates ---------------------------
+
+def _streams(rng, S, n, tau, scale=1.5e-3):
+    """S workers' encodes of their own gradients; [S][n] words, counts."""
+    words = np.zeros((S, n), np.uint32)
+    counts = np.zeros(S, np.int64)
+    rs, gs = [], []
+    for s in range(S):
+        g = (rng.integers(-6000, 6000, n) * 2.0 ** -22).astype(np.float32)
+        r = (rng.integers(-1000, 1000, n) * 2.0 ** -22).astype(np.float32)
+        new_r, w, c = oracle.grad_threshold_encode(g, r, tau)
+        words[s, :c] = w
+        words[s, c:] = 0xFFFFFFFF  # garbage past the count
+        counts[s] = c
+        rs.append((r, g, new_r))
+    return words, counts, rs
+
+
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_decode_multi_single_stream_is_decode(accumulate):
+    rng = np.random.default_rng(20)
+    n, tau = 20_000, np.float32(1e-3)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    _, w, c = oracle.grad_threshold_encode(g, np.zeros(n, np.float32), tau)
+    base = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    a = oracle.grad_threshold_decode(w, c, tau, n, base, accumulate)
+    b = oracle.grad_threshold_decode_multi(w[None, :], [c], tau, n, base, accumulate)
+    np.testing.assert_array_equal(_bits(a), _bits(b))
+
+
+def test_decode_multi_equals_sum_of_single_decodes():
+    # tau a power of two: each single decode is exact, their fp64 sum too
+    rng = np.random.default_rng(21)
+    n, S, tau = 30_000, 6, np.float32(2.0 ** -10)
+    words, counts, _ = _streams(rng, S, n, tau)
+    total = np.zeros(n, np.float64)
+    for s in range(S):
+        total += oracle.grad_threshold_decode(words[s], counts[s], tau, n).astype(np.float64)
+    agg = oracle.grad_threshold_decode_multi(words, counts, tau, n)
+    np.testing.assert_array_equal(agg.astype(np.float64), total)
+    assert np.count_nonzero(np.abs(total) > tau) > 0  # some indices sent by several workers
+
+
+def test_decode_multi_is_order_independent():
+    rng = np.random.default_rng(22)
+    n, S, tau = 10_000, 5, np.float32(1e-3)
+    words, counts, _ = _streams(rng, S, n, tau)
+    base = (rng.standard_normal(n) * 1e-2).astype(np.float32)
+    a = oracle.grad_threshold_decode_multi(words, counts, tau, n, base, True)
+    perm = rng.permutation(S)
+    b = oracle.grad_threshold_decode_multi(words[perm], counts[perm], tau, n, base, True)
+    np.testing.assert_array_equal(_bits(a), _bits(b))
+
+
+def test_decode_multi_conserves_across_workers():
+    # sum over workers of (kept + sent) equals sum of (residual + gradient),
+    # exactly on the power-of-two grid
+    rng = np.random.default_rng(23)
+    n, S, tau = 25_000, 4, np.float32(2.0 ** -10)
+    words, counts, rs = _streams(rng, S, n, tau)
+    agg = oracle.grad_threshold_decode_multi(words, counts, tau, n).astype(np.float64)
+    kept = sum(x[2].astype(np.float64) for x in rs)
+    came = sum(x[0].astype(np.float64) + x[1].astype(np.float64) for x in rs)
+    np.testing.assert_array_equal(kept + agg, came)
+
+
+def test_decode_multi_cancelling_signs():
+    n, tau = 8, np.float32(0.25)
+    words = np.array([[(3 << 1) | 0, (5 << 1) | 0], [(3 << 1) | 1, (5 << 1) | 0]], np.uint32)
+    out = oracle.grad_threshold_decode_multi(words, [2, 2], tau, n)
+    np.testing.assert_array_equal(out, np.array([0, 0, 0, 0, 0, 0.5, 0, 0], np.float32))
+    assert not np.signbit(out[3])
+    base = np.full(n, 1.0, np.float32)
+    acc = oracle.grad_threshold_decode_multi(words, [2, 2], tau, n, base, True)
+    np.testing.assert_array_equal(acc, np.array([1, 1, 1, 1, 1, 1.5, 1, 1], np.float32))
+    # accumulate leaves elements no word names untouched, -0.0 included
+    negz = np.full(n, -0.0, np.float32)
+    acc = oracle.grad_threshold_decode_multi(words, [2, 2], tau, n, negz, True)
+    assert np.all(np.signbit(acc[[0, 1, 2, 4, 6, 7]]))
+    assert not np.signbit(acc[3]) and acc[5] == 0.5

@@ -140,3 +140,63 @@ def test_unmutated_oracle_passes_gtc_pins():
 ])
 def test_gtc_mistakes_are_caught(old, new):
     assert not _gtc_pins_pass(_mutant("gtc.py", old, new))
+
+
+# ---- BMUF and the multi-worker aggregate ------------------------------------
+
+@pytest.mark.parametrize("old,new", [
+    ("new_w = (wg + d) + eta_next * d", "new_w = (wg + d)"),               # look-ahead dropped
+    ("new_w = (wg + d) + eta_next * d", "new_w = (wg + d) + eta * d"),     # wrong momentum index
+    ("g = wbar - wg", "g = wg - wbar"),                                    # wrong sign of G
+    ("wbar = s / np.float64(workers)", "wbar = s / np.float64(m.shape[0])"),  # averages the addends
+    ("d = eta * d0 + zeta * g", "d = eta * g + zeta * g"),                 # momentum forgets Delta
+])
+def test_bmuf_pins_reject(old, new):
+    import tests.test_oracle_bmuf as pins
+    mod = _mutant("bmuf.py", old, new)
+    saved = oracle.bmuf_block_update
+    oracle.bmuf_block_update = mod.bmuf_block_update
+    try:
+        failures = 0
+        for name in ("test_single_worker_without_momentum_takes_the_local_model",
+                     "test_block_momentum_closed_form_over_blocks",
+                     "test_look_ahead_uses_the_next_momentum",
+                     "test_all_reduced_sum_gives_the_same_step"):
+            try:
+                getattr(pins, name)()
+            except AssertionError:
+                failures += 1
+        for w in (2, 4, 8):
+            try:
+                pins.test_without_momentum_is_model_averaging(w)
+            except AssertionError:
+                failures += 1
+        assert failures > 0, (old, new)
+    finally:
+        oracle.bmuf_block_update = saved
+
+
+@pytest.mark.parametrize("old,new", [
+    ("sign = np.where((ws & np.uint32(1)) != 0, -1, 1)", "sign = np.where((ws & np.uint32(1)) != 0, 1, -1)"),
+    ("ws = w[s, :int(counts[s])]", "ws = w[s, :int(counts[s])][:-1]"),       # last word lost
+    ("out[hit] = out[hit] + v[hit]", "out = out + v"),                     # touches unsent elements
+])
+def test_decode_multi_pins_reject(old, new):
+    import tests.test_oracle_gtc as pins
+    mod = _mutant("gtc.py", old, new)
+    saved = oracle.grad_threshold_decode_multi
+    oracle.grad_threshold_decode_multi = mod.grad_threshold_decode_multi
+    try:
+        failures = 0
+        for call in (lambda: pins.test_decode_multi_single_stream_is_decode(False),
+                     lambda: pins.test_decode_multi_single_stream_is_decode(True),
+                     pins.test_decode_multi_equals_sum_of_single_decodes,
+                     pins.test_decode_multi_conserves_across_workers,
+                     pins.test_decode_multi_cancelling_signs):
+            try:
+                call()
+            except AssertionError:
+                failures += 1
+        assert failures > 0, (old, new)
+    finally:
+        oracle.grad_threshold_decode_multi = saved
