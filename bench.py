@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="paper-5x768")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-worker-kernels", action="store_true",
+                    help="skip timing the multi-worker pieces (BMUF step, 8-stream aggregate)")
     ap.add_argument("--cpu-chunks", type=int, default=0,
                     help="chunks the CPU oracle runs forward/backward on (0 = the whole batch)")
     return ap.parse_args()
@@ -108,6 +110,68 @@ def step_flops(w, T, lengths):
     return per_frame * N, N
 
 
+def _hbm_entry(kt, reps):
+    us = kt["ms"] * 1e3 / max(kt["launches"], 1)
+    per_launch = kt["bytes"] / max(kt["launches"], 1)
+    gbs = per_launch / (us * 1e-6) / 1e9
+    return {"us_per_launch": round(us, 2), "algorithmic_bytes_per_launch": per_launch,
+            "achieved_GBs": round(gbs, 1), "peak_GBs": PEAK_HBM_GBS,
+            "frac": round(gbs / PEAK_HBM_GBS, 4), "launches": kt["launches"]}
+
+
+def worker_kernels(am, n, reps):
+    """Per-GPU pieces of the multi-worker trainers on the step's flat model
+    (outside the timed step): the BMUF-NBM global step over 8 local models
+    with the restart copies, and the aggregate of 8 workers' compressed
+    updates at about a 1 % send rate.  Each launch is timed with HIP events;
+    inputs stay resident in HBM (8 models = 773 MB, more than the 256 MB
+    Infinity Cache)."""
+    import torch
+    dev = torch.device("cuda")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5)
+    S = 8
+    out = {}
+    # BMUF: N = 8 local models, eta = 0.875, zeta = C N (1 - eta) with C = 1
+    base = torch.rand(n, generator=gen, device=dev) * 0.07 - 0.035
+    models = base[None, :] + torch.randn((S, n), generator=gen, device=dev) * 1e-3
+    wg = base.clone()
+    delta = torch.zeros(n, device=dev)
+    local = torch.empty(n, device=dev)
+    local_bf = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    am.profile_begin([am.K_BMUF])
+    for _ in range(reps):
+        am.bmuf_block_update(models, S, wg, delta, 0.875, 0.875, 1.0, local, local_bf)
+    am.profile_end()
+    out["bmuf_update"] = dict(_hbm_entry(am.profile_get(am.K_BMUF), reps), workers=S,
+                              bytes_per_element=4 * S + 16 + 6)
+    del models, base, wg, delta, local, local_bf
+    # aggregate of 8 streams: each worker's encode of N(0, sigma^2) gradients
+    # with tau / sigma = 2.576 (a 1 % send rate), words [8][n]
+    tau = 1e-4
+    words = torch.zeros((S, n), dtype=torch.int32, device=dev)
+    counts = torch.zeros(S, dtype=torch.int64, device=dev)
+    ews = torch.zeros(am.encode_workspace_bytes(n), dtype=torch.uint8, device=dev)
+    for s in range(S):
+        g = torch.randn(n, generator=gen, device=dev) * (tau / 2.576)
+        r = torch.zeros(n, device=dev)
+        am.grad_threshold_encode(g, r, tau, words[s], counts[s:s + 1], ews)
+    dense = torch.empty(n, device=dev)
+    dws = torch.zeros(am.decode_multi_workspace_bytes(S, n), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    total_words = int(counts.sum())
+    am.profile_begin([am.K_DECODE])
+    for _ in range(reps):
+        am.grad_threshold_decode_multi(words, counts, tau, dense, dws)
+    am.profile_end()
+    kt = am.profile_get(am.K_DECODE)
+    # algorithmic bytes: every word read once, the dense update written once
+    kt = dict(kt, bytes=(4.0 * n + 4.0 * total_words) * kt["launches"])
+    out["decode_multi"] = dict(_hbm_entry(kt, reps), streams=S, words=total_words)
+    return out
+
+
 def cpu_baseline(wl, synth, chunks):
     """The oracle, as it stands, on a bounded sample: forward, CE and BPTT on
     `chunks` chunks of the batch, plus encode, decode and SGD of the whole
@@ -164,11 +228,12 @@ def main():
     for _ in range(args.warmup):
         st.step()
     torch.cuda.synchronize()
-    am.profile_begin(range(10))
+    classes = range(len(am.KERNEL_CLASSES))
+    am.profile_begin(classes)
     st.step()
     am.profile_end()
-    totals = {k: am.profile_get(k) for k in range(10)}
-    dom = max(range(10), key=lambda k: totals[k]["ms"])
+    totals = {k: am.profile_get(k) for k in classes}
+    dom = max(classes, key=lambda k: totals[k]["ms"])
     torch.cuda.synchronize()
 
     # timed steps; the dominant class is bracketed by HIP events on its stream
@@ -229,8 +294,11 @@ def main():
             (PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS) * 1e12), 2),
         "step_tflop": round(flops / 1e12, 4),
         "roofline": roof,
-        "kernel_ms_per_step": {am.KERNEL_CLASSES[k]: round(totals[k]["ms"], 3) for k in range(10)},
+        "kernel_ms_per_step": {am.KERNEL_CLASSES[k]: round(totals[k]["ms"], 3) for k in classes
+                               if totals[k]["launches"] > 0},
     }
+    if not args.no_worker_kernels:
+        out["worker_kernels"] = worker_kernels(am, st.n, reps=10)
     if not args.no_cpu_baseline and args.workload in ("paper-5x768", "tiny-2x64", "wide-5x1536"):
         out["cpu_baseline"] = cpu_baseline(args.workload, synth, args.cpu_chunks)
     print(json.dumps(out), flush=True)

@@ -7,6 +7,9 @@
  * chunked BPTT (§II-B, §V-D) against sparse k-best teacher posteriors
  * (§II-C, §V-C) by mini-batch SGD (§VI, §VI-B), whose gradient is passed
  * through Gradient Threshold Compression with residual error feedback (§VI-A).
+ * Two pieces of the multi-worker trainers run per GPU as well: the aggregate
+ * of several workers' compressed updates (§VI-A) and the BMUF-NBM global
+ * model step (§VI-B).
  *
  * Conventions for every entry point:
  *  - Pointers are device pointers unless the comment says [host].
@@ -164,6 +167,46 @@ am_status grad_threshold_decode(const uint32_t* words, const int64_t* count, int
                                 float tau, int64_t n, float* dense, int32_t accumulate,
                                 void* stream);
 
+/* Aggregate of the sparse updates of several workers (§VI-A: each worker
+ * receives every other worker's sparse update and aggregates them).  Stream
+ * s is row s of `words` [streams][capacity] (for example the result of a
+ * fixed-capacity all-gather of each worker's encode output) holding
+ * min(counts[s], capacity) valid words, strictly ascending in index as
+ * encode writes them; counts [streams] are device int64.  With k_i = the
+ * sum over all streams of +1 (sign bit 0) or -1 (sign bit 1) for the words
+ * naming element i, computed exactly in integers (so the result does not
+ * depend on the order of the streams), and q_i = tau * k_i rounded once to
+ * fp32:
+ *   accumulate = 0: dense[i] = q_i where some word names i, else +0.0;
+ *   accumulate = 1: dense[i] = fl32(dense[i] + q_i) where some word names i,
+ *                   other elements unchanged.
+ * With one stream this equals grad_threshold_decode.  n < 2^31,
+ * 0 <= streams <= 32767; workspace: am_decode_multi_workspace_bytes.        */
+int64_t am_decode_multi_workspace_bytes(int32_t streams, int64_t n);
+am_status grad_threshold_decode_multi(int32_t streams, const uint32_t* words, int64_t capacity,
+                                      const int64_t* counts, float tau, int64_t n, float* dense,
+                                      int32_t accumulate, void* ws, int64_t ws_bytes,
+                                      void* stream);
+
+/* BMUF-NBM global step that ends a block of local SGD (§VI-B, eqs. (1)-(4)),
+ * per element i, in fp64 from the fp32 inputs, in this order, without fused
+ * multiply-adds, each output rounded once to fp32:
+ *   Wbar  = (models[0][i] + models[1][i] + ... + models[count-1][i]) / workers
+ *   G     = Wbar - global_model[i]
+ *   Delta = eta * delta[i] + zeta * G                     (eta = eta_t, zeta = zeta_t)
+ *   W     = (global_model[i] + Delta) + eta_next * Delta  (eta_next = eta_{t+1})
+ *   global_model[i] = W;  delta[i] = Delta;
+ *   local_master[i] = W (or NULL);  local_bf16[i] = RNE bf16 of W (or NULL).
+ * models: `count` fp32 rows `model_stride` elements apart: the N local
+ * models (count = workers = N), or their all-reduced sum (count = 1,
+ * workers = N).  Eq. (5) sets zeta = C N (1 - eta) for a constant C >= 1.
+ * Each output may alias an input at the same index (in-place state, or the
+ * restart copy written over an addend).                                    */
+am_status bmuf_block_update(int64_t n, int32_t count, int32_t workers, const float* models,
+                            int64_t model_stride, float* global_model, float* delta, float eta,
+                            float eta_next, float zeta, float* local_master, void* local_bf16,
+                            void* stream);
+
 /* Local SGD step (§VI, §VI-B): master[i] = fl32(master[i] - lr * update[i])
  * evaluated in fp64; weights_bf16[i] (uint16 bit patterns, or NULL) =
  * round-to-nearest-even bf16 of the new master (NaN -> 0x7FC0).           */
@@ -187,7 +230,8 @@ typedef enum {
   AM_K_DECODE = 7,
   AM_K_SGD = 8,
   AM_K_MISC = 9,          /* casts, transposes, bias reductions, gathers */
-  AM_K_NCLASSES = 10
+  AM_K_BMUF = 10,         /* BMUF-NBM global step */
+  AM_K_NCLASSES = 11
 } am_kernel_class;
 
 /* Starts recording: every later launch of a class whose bit is set in

@@ -19,9 +19,9 @@ LIB_PATH = os.path.join(HERE, "libmi355am.so")
 F32, BF16 = 0, 1
 MEAN_VALID, SUM = 0, 1
 K_GEMM_FWD, K_GEMM_BWD_DATA, K_GEMM_BWD_WGT, K_LSTM_FWD, K_LSTM_BWD = 0, 1, 2, 3, 4
-K_CE, K_ENCODE, K_DECODE, K_SGD, K_MISC = 5, 6, 7, 8, 9
+K_CE, K_ENCODE, K_DECODE, K_SGD, K_MISC, K_BMUF = 5, 6, 7, 8, 9, 10
 KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd_data", "gemm_bwd_wgt", "lstm_fwd", "lstm_bwd",
-                  "soft_ce", "encode", "decode", "sgd", "misc"]
+                  "soft_ce", "encode", "decode", "sgd", "misc", "bmuf"]
 
 
 class AmError(RuntimeError):
@@ -66,6 +66,9 @@ _PROTOS = {
     "grad_threshold_encode": (_I32, [_I64, _P, _P, _F32, _P, _I64, _P, _P, _I64, _P]),
     "grad_threshold_decode": (_I32, [_P, _P, _I64, _F32, _I64, _P, _I32, _P]),
     "sgd_apply": (_I32, [_I64, _P, _P, _P, _F32, _P]),
+    "am_decode_multi_workspace_bytes": (_I64, [_I32, _I64]),
+    "grad_threshold_decode_multi": (_I32, [_I32, _P, _I64, _P, _F32, _I64, _P, _I32, _P, _I64, _P]),
+    "bmuf_block_update": (_I32, [_I64, _I32, _I32, _P, _I64, _P, _P, _F32, _F32, _F32, _P, _P, _P]),
     "am_cast_f32_to_bf16": (_I32, [_I64, _P, _P, _P]),
     "am_workspace_check": (_I32, [_P, _I64, _P]),
     "am_profile_begin": (_I32, [ctypes.c_uint32]),
@@ -213,6 +216,36 @@ def grad_threshold_decode(words, count, tau, dense, accumulate=False, stream=Non
         _dev(words, "words", torch.int32), _dev(count, "count", torch.int64), words.numel(),
         float(tau), dense.numel(), _dev(dense, "dense", torch.float32), int(bool(accumulate)),
         _stream(stream)))
+
+
+def decode_multi_workspace_bytes(streams, n) -> int:
+    return int(lib().am_decode_multi_workspace_bytes(streams, n))
+
+
+def grad_threshold_decode_multi(words, counts, tau, dense, ws, accumulate=False, stream=None):
+    """words: [streams][capacity] int32 GPU tensor; counts: [streams] int64."""
+    if words.dim() != 2:
+        raise AmError("words must be [streams][capacity]")
+    S, cap = words.shape
+    _check(lib().grad_threshold_decode_multi(
+        S, _dev(words, "words", torch.int32), cap, _dev(counts, "counts", torch.int64),
+        float(tau), dense.numel(), _dev(dense, "dense", torch.float32), int(bool(accumulate)),
+        _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def bmuf_block_update(models, workers, global_model, delta, eta, eta_next, zeta,
+                      local_master=None, local_bf16=None, stream=None):
+    """models: [count][n] (or [n]) fp32 GPU tensor of the average's addends."""
+    m2 = models if models.dim() == 2 else models.view(1, -1)
+    count, n = m2.shape
+    if global_model.numel() != n or delta.numel() != n:
+        raise AmError("global_model and delta must hold n elements")
+    _check(lib().bmuf_block_update(
+        n, count, int(workers), _dev(m2, "models", torch.float32), n,
+        _dev(global_model, "global_model", torch.float32), _dev(delta, "delta", torch.float32),
+        float(eta), float(eta_next), float(zeta),
+        _dev(local_master, "local_master", torch.float32),
+        _dev(local_bf16, "local_bf16", torch.bfloat16), _stream(stream)))
 
 
 def sgd_apply(master, update, lr, weights_bf16=None, stream=None):

@@ -141,6 +141,16 @@ hipError_t gtc_encode(int64_t n, const float* g, float* r, float tau, uint32_t* 
                       int64_t* count, uint32_t* ws_mask, int32_t* ws_tile, hipStream_t s);
 hipError_t gtc_decode(const uint32_t* words, const int64_t* count, int64_t capacity, float tau,
                       int64_t n, float* dense, bool accumulate, hipStream_t s);
+// Aggregate of `streams` workers' streams, words [streams][capacity];
+// ws_start holds streams x (gtc_tiles(n) + 1) int32.
+hipError_t gtc_decode_multi(int streams, const uint32_t* words, int64_t capacity,
+                            const int64_t* counts, float tau, int64_t n, float* dense,
+                            bool accumulate, int32_t* ws_start, hipStream_t s);
+
+// BMUF-NBM global step (count addends of stride elements, divided by workers).
+hipError_t bmuf_update(int64_t n, int count, int workers, const float* models, int64_t stride,
+                       float* wg, float* delta, float eta, float eta_next, float zeta,
+                       float* local, uint16_t* local_bf16, hipStream_t s);
 
 // Elementwise and data-movement helpers.
 hipError_t sgd_apply_f32(int64_t n, float* master, uint16_t* w_bf16, const float* u, float lr,

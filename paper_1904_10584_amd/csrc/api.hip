@@ -408,6 +408,49 @@ am_status grad_threshold_decode(const uint32_t* words, const int64_t* count, int
   return hip_check(am::gtc_decode(words, count, capacity, tau, n, dense, accumulate != 0, s), "decode");
 }
 
+int64_t am_decode_multi_workspace_bytes(int32_t streams, int64_t n) {
+  if (streams < 0 || n < 0) return -1;
+  return align256((int64_t)streams * (am::gtc_tiles(n) + 1) * 4);
+}
+
+am_status grad_threshold_decode_multi(int32_t streams, const uint32_t* words, int64_t capacity,
+                                      const int64_t* counts, float tau, int64_t n, float* dense,
+                                      int32_t accumulate, void* ws, int64_t ws_bytes,
+                                      void* stream) {
+  if (n < 0 || n >= (1ll << 31)) return fail(AM_EINVAL, "n outside [0, 2^31)");
+  if (streams < 0 || streams > 32767) return fail(AM_EINVAL, "streams outside [0, 32767]");
+  if (capacity < 0) return fail(AM_EINVAL, "capacity < 0");
+  if ((n > 0 && !dense) || (streams > 0 && (!counts || (capacity > 0 && !words))))
+    return fail(AM_EINVAL, "NULL pointer");
+  if (accumulate != 0 && accumulate != 1) return fail(AM_EINVAL, "accumulate must be 0 or 1");
+  const int64_t need = am_decode_multi_workspace_bytes(streams, n);
+  if (need > 0 && (!ws || ws_bytes < need || !aligned(ws, 256)))
+    return fail(AM_EWORKSPACE, "multi-stream decode needs %lld workspace bytes (256-aligned)",
+                (long long)need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Timed tm(AM_K_DECODE, s, 0.0, (accumulate ? 8.0 : 4.0) * n);
+  return hip_check(am::gtc_decode_multi(streams, words, capacity, counts, tau, n, dense,
+                                        accumulate != 0, static_cast<int32_t*>(ws), s),
+                   "multi-stream decode");
+}
+
+am_status bmuf_block_update(int64_t n, int32_t count, int32_t workers, const float* models,
+                            int64_t model_stride, float* global_model, float* delta, float eta,
+                            float eta_next, float zeta, float* local_master, void* local_bf16,
+                            void* stream) {
+  if (n < 0) return fail(AM_EINVAL, "n < 0");
+  if (count < 1 || workers < 1) return fail(AM_EINVAL, "count and workers must be >= 1");
+  if (count > 1 && model_stride < n) return fail(AM_EINVAL, "model_stride < n");
+  if (n > 0 && (!models || !global_model || !delta)) return fail(AM_EINVAL, "NULL pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const double bytes = (4.0 * count + 16.0 + (local_master ? 4.0 : 0.0) + (local_bf16 ? 2.0 : 0.0)) * n;
+  Timed tm(AM_K_BMUF, s, 0.0, bytes);
+  return hip_check(am::bmuf_update(n, count, workers, models, model_stride, global_model, delta,
+                                   eta, eta_next, zeta, local_master,
+                                   static_cast<uint16_t*>(local_bf16), s),
+                   "bmuf_block_update");
+}
+
 am_status sparse_soft_ce(int64_t N, int32_t C, int32_t K, const float* logits, const int32_t* idx,
                          const float* prob, const uint8_t* mask, int32_t reduction, float* loss,
                          void* dlogits, int32_t dlogits_dtype, void* ws, int64_t ws_bytes,

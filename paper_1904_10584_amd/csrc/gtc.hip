@@ -12,7 +12,9 @@
 //      in index order and writes their words contiguously.
 // Decode builds each 4096-element tile of the dense update in LDS (zero or
 // the existing values, then +-tau at the indices of the tile's words, found
-// by binary search in the ascending word list) and writes it once.
+// by binary search in the ascending word list) and writes it once.  The
+// aggregate of several workers' streams (below) counts signs per element in
+// LDS integers and scales by tau once.
 #include "am_device.h"
 #include "am_internal.h"
 
@@ -184,6 +186,74 @@ __global__ __launch_bounds__(TPB) void gtc_decode_tiles(const uint32_t* __restri
   for (int i = threadIdx.x; i < len; i += TPB) dense[base + i] = tile[i];
 }
 
+
+// ---- aggregate of several workers' streams ----------------------------------
+// Streams are the rows of words [S][capacity], each ascending in index.  A
+// bounds pass finds, for every stream s and tile t, the first word of s at or
+// after the tile by binary search (start[s][t], t = 0..ntiles);
+// then each tile adds (1 << 16) +- 1 per word into an LDS integer per
+// element (hits in the upper half, the signed sum k in the lower), and writes
+// fl32(tau * k) where some word named the element.  Integer adds commute, so
+// the result does not depend on the order of the streams or of the words.
+
+__global__ __launch_bounds__(TPB) void gtc_multi_bounds(const uint32_t* __restrict__ words,
+                                                        int64_t capacity,
+                                                        const int64_t* __restrict__ counts,
+                                                        int64_t ntiles, int64_t n,
+                                                        int32_t* __restrict__ start) {
+  const int s = blockIdx.y;
+  const int64_t t = (int64_t)blockIdx.x * TPB + threadIdx.x;
+  if (t > ntiles) return;
+  int64_t cnt = counts[s];
+  cnt = cnt < 0 ? 0 : (cnt > capacity ? capacity : cnt);
+  const int64_t first = t * TILE < n ? t * TILE : n;  // n < 2^31: the key fits
+  start[(int64_t)s * (ntiles + 1) + t] =
+      (int32_t)lower_bound_words(words + (int64_t)s * capacity, cnt, (uint32_t)(first << 1));
+}
+
+template <bool ACC>
+__global__ __launch_bounds__(TPB) void gtc_multi_tiles(const uint32_t* __restrict__ words,
+                                                       int64_t capacity,
+                                                       const int64_t* __restrict__ counts,
+                                                       int streams,
+                                                       const int32_t* __restrict__ start,
+                                                       int64_t ntiles, float tau, int64_t n,
+                                                       float* __restrict__ dense) {
+  __shared__ int acc[TILE];
+  const int64_t t = blockIdx.x, base = t * TILE;
+  const int len = (int)(n - base < TILE ? n - base : TILE);
+  for (int i = threadIdx.x; i < TILE; i += TPB) acc[i] = 0;
+  __syncthreads();
+  for (int s = 0; s < streams; ++s) {
+    int64_t cnt = counts[s];
+    cnt = cnt < 0 ? 0 : (cnt > capacity ? capacity : cnt);
+    const int32_t* st = start + (int64_t)s * (ntiles + 1);
+    int64_t lo = st[t], hi = st[t + 1];
+    lo = lo < 0 ? 0 : (lo > cnt ? cnt : lo);
+    hi = hi < lo ? lo : (hi > cnt ? cnt : hi);
+    const uint32_t* w = words + (int64_t)s * capacity;
+    for (int64_t p = lo + threadIdx.x; p < hi; p += TPB) {
+      const uint32_t word = w[p];
+      const int i = (int)((word >> 1) - (uint32_t)base);
+      if ((unsigned)i >= (unsigned)len) continue;  // only for malformed streams
+      atomicAdd(&acc[i], (word & 1u) ? (1 << 16) - 1 : (1 << 16) + 1);
+    }
+  }
+  __syncthreads();
+  const double tau64 = (double)tau;
+  for (int i = threadIdx.x; i < len; i += TPB) {
+    const int v = acc[i];
+    const int hits = (v + 32768) >> 16;
+    const int k = v - (hits << 16);
+    if (hits > 0) {
+      const float q = (float)(tau64 * (double)k);
+      dense[base + i] = ACC ? dense[base + i] + q : q;
+    } else if (!ACC) {
+      dense[base + i] = 0.f;
+    }
+  }
+}
+
 }  // namespace
 
 int64_t gtc_tiles(int64_t n) { return (n + TILE - 1) / TILE; }
@@ -217,6 +287,28 @@ hipError_t gtc_decode(const uint32_t* words, const int64_t* count, int64_t capac
   else
     hipLaunchKernelGGL(gtc_decode_tiles<false>, dim3((unsigned)ntiles), dim3(TPB), 0, s, words,
                        count, capacity, tau, n, dense);
+  return hipGetLastError();
+}
+
+}  // namespace am
+
+namespace am {
+
+hipError_t gtc_decode_multi(int streams, const uint32_t* words, int64_t capacity,
+                            const int64_t* counts, float tau, int64_t n, float* dense,
+                            bool accumulate, int32_t* ws_start, hipStream_t s) {
+  const int64_t ntiles = gtc_tiles(n);
+  if (ntiles == 0) return hipSuccess;
+  if (streams == 0) return accumulate ? hipSuccess : fill_zero(dense, n, s);
+  const unsigned bx = (unsigned)((ntiles + 1 + TPB - 1) / TPB);
+  hipLaunchKernelGGL(gtc_multi_bounds, dim3(bx, (unsigned)streams), dim3(TPB), 0, s, words,
+                     capacity, counts, ntiles, n, ws_start);
+  if (accumulate)
+    hipLaunchKernelGGL(gtc_multi_tiles<true>, dim3((unsigned)ntiles), dim3(TPB), 0, s, words,
+                       capacity, counts, streams, ws_start, ntiles, tau, n, dense);
+  else
+    hipLaunchKernelGGL(gtc_multi_tiles<false>, dim3((unsigned)ntiles), dim3(TPB), 0, s, words,
+                       capacity, counts, streams, ws_start, ntiles, tau, n, dense);
   return hipGetLastError();
 }
 

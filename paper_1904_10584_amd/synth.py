@@ -12,12 +12,19 @@ Stand-ins for data the paper trains on (Alexa production speech, not public):
   * chunks: fixed-length chunks for chunked BPTT (§II-B) or whole utterances of
     varying length, sorted longest first.
 
-Seeds: weights 0, features 1, targets 2, lengths 3, one-hot frame choice 4.
+Stand-ins for the state of several data-parallel workers (one GPU plays all
+of them): local models that drifted from the global model over a block of
+local SGD (the global model plus N(0, spread^2) noise per worker), and
+per-worker gradients of the scale of the training step's (N(0, scale^2)).
+
+Seeds: weights 0, features 1, targets 2, lengths 3, one-hot frame choice 4,
+worker models 5, worker gradients 6.
 """
 
 import numpy as np
 
 SEED_WEIGHTS, SEED_FEATURES, SEED_TARGETS, SEED_LENGTHS, SEED_ONEHOT = 0, 1, 2, 3, 4
+SEED_WORKER_MODELS, SEED_WORKER_GRADS = 5, 6
 
 # Workload shapes.  dtype "f32": fp32 throughout; "bf16": bf16 weights and
 # activations with fp32 master weights.
@@ -80,3 +87,19 @@ def teacher_targets(n_frames, classes, k, mass, seed=SEED_TARGETS, zipf_s=1.1,
         prob[sel, 0] = 1.0
         prob[sel, 1:] = 0.0
     return idx, prob
+
+
+def worker_models(base, workers, spread, seed=SEED_WORKER_MODELS):
+    """[workers][n] fp32: base plus independent N(0, spread^2) drift per worker."""
+    rng = np.random.default_rng(seed)
+    base = np.asarray(base, dtype=np.float32)
+    out = np.empty((workers, base.shape[0]), dtype=np.float32)
+    for i in range(workers):
+        out[i] = base + (rng.standard_normal(base.shape[0], dtype=np.float32) * np.float32(spread))
+    return out
+
+
+def worker_gradients(n, workers, scale, seed=SEED_WORKER_GRADS):
+    """[workers][n] fp32 gradients, i.i.d. N(0, scale^2)."""
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal((workers, n), dtype=np.float32) * np.float32(scale))

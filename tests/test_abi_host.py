@@ -138,3 +138,32 @@ def test_workspace_queries_are_monotone(L):
     assert a > b > 0 and a % 256 == 0
     assert L.am_workspace_bytes(ctypes.byref(m), 64, 256, 64 * 256 + 1) == -1
     assert L.am_encode_workspace_bytes(24_145_848) > L.am_encode_workspace_bytes(1000) > 0
+
+
+def test_bmuf_and_multi_decode_argument_checks(L):
+    fake = ctypes.c_void_p(0x100000)
+    f = ctypes.c_float
+    # bmuf: counts, stride, NULLs
+    st, _ = _status(L, "bmuf_block_update", 100, 0, 1, fake, 100, fake, fake, f(0.5), f(0.5), f(1.0), None, None, None)
+    assert st == -1
+    st, _ = _status(L, "bmuf_block_update", 100, 2, 2, fake, 99, fake, fake, f(0.5), f(0.5), f(1.0), None, None, None)
+    assert st == -1
+    st, _ = _status(L, "bmuf_block_update", 100, 1, 0, fake, 100, fake, fake, f(0.5), f(0.5), f(1.0), None, None, None)
+    assert st == -1
+    st, _ = _status(L, "bmuf_block_update", 100, 1, 1, None, 100, fake, fake, f(0.5), f(0.5), f(1.0), None, None, None)
+    assert st == -1
+    # multi-stream decode: stream count, workspace, NULLs, accumulate flag
+    n = 50_000
+    ws = L.am_decode_multi_workspace_bytes(4, n)
+    assert ws >= 4 * ((n + 4095) // 4096 + 1) * 4 and ws % 256 == 0
+    assert L.am_decode_multi_workspace_bytes(-1, n) == -1
+    st, _ = _status(L, "grad_threshold_decode_multi", 40000, fake, n, fake, f(1e-3), n, fake, 0, fake, 1 << 30, None)
+    assert st == -1
+    st, _ = _status(L, "grad_threshold_decode_multi", 4, fake, n, fake, f(1e-3), n, fake, 0, fake, ws - 1, None)
+    assert st == -5
+    st, _ = _status(L, "grad_threshold_decode_multi", 4, fake, n, None, f(1e-3), n, fake, 0, fake, ws, None)
+    assert st == -1
+    st, _ = _status(L, "grad_threshold_decode_multi", 4, fake, n, fake, f(1e-3), n, fake, 2, fake, ws, None)
+    assert st == -1
+    st, _ = _status(L, "grad_threshold_decode_multi", 4, fake, n, fake, f(1e-3), 1 << 31, fake, 0, fake, ws, None)
+    assert st == -1
