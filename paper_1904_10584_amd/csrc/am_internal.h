@@ -71,7 +71,7 @@ struct LstmBwdStep {
 };
 hipError_t lstm_bwd_step(const LstmBwdStep& a, hipStream_t s);
 
-// Persistent layer kernels (all time steps in one cooperative launch).
+// Persistent layer kernels (all time steps in one launch of a resident grid).
 // The schedule of a batch: T steps, B sequences, N frames; with varlen the
 // sorted lengths (B <= 1024), else every sequence has T frames.
 struct PersistSchedule {
@@ -114,6 +114,15 @@ struct XcdSync {
   int units;  // filled in by the launcher
 };
 bool lstm_xcd_instantiated(bool forward, int hidden, int B);
+// Launch of a grid that the caller has checked fits on the device at once
+// (occupancy x CUs).  With AM_COOPERATIVE=1 in the environment it goes
+// through the cooperative launch (which guarantees co-residency but adds
+// about 25 us of dispatch overhead around each launch); otherwise it is an
+// ordinary launch, whose workgroups are all resident on an otherwise idle
+// device, and every step barrier is bounded, so a grid that is not resident
+// ends in the barrier time-out flag, never in a hang.
+hipError_t resident_launch(const void* fn, dim3 grid, dim3 block, void** args, size_t lds,
+                           hipStream_t s);
 hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used);
 hipError_t lstm_bwd_xcd_launch(PersistBwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used);
 

@@ -154,12 +154,101 @@ template <typename OutT> struct Out {
   int64_t zstride;  // elements between the outputs of consecutive k-splits
 };
 
+// Epilogue through LDS.  The accumulators of a 16x16 MFMA tile sit as four
+// rows of one column per lane, so storing them straight to a row-major
+// output takes one 2- or 4-byte store per element (1024 store instructions
+// per 256x256 bf16 tile), which is slower than the tile's products.  Here
+// the waves write their tiles to LDS in the output's row-major order (the
+// stage buffers are free once the k-loop is done), then every thread copies
+// whole 16-byte chunks of rows to global memory.  bf16: adjacent lanes swap
+// half their values (a DPP swap) so each lane writes 4-byte pairs of
+// columns.  LDS rows are BN elements; the 16-byte chunks of row R are
+// XOR-permuted by (R / 4) % 4 times 32 bytes, so the four row groups one
+// write instruction touches fall in different banks.  fp32 tiles go through
+// LDS in two passes of 128 rows.  Requires (checked by the launcher) output
+// row pitches and the column split a multiple of 16 bytes and N of the
+// chunk width.
+template <typename OutT, int BN, bool BIAS>
+__device__ __forceinline__ void store_tile_staged(const f32x4_t (&acc)[BM / 2 / 16][BN / 4 / 16],
+                                                  const Out<OutT>& C, const bf16_t* bias,
+                                                  bf16_t* smem, int M, int N, int m0, int n0,
+                                                  int z, int wm, int wn, int wave, int lane) {
+  constexpr int MI = BM / 2 / 16, NJ = BN / 4 / 16;
+  constexpr int ES = sizeof(OutT);
+  constexpr int ROWB = BN * ES;              // LDS bytes per tile row
+  constexpr int CPR = ROWB / 16;             // 16-byte chunks per row
+  constexpr int EPC = 16 / ES;               // elements per chunk
+  constexpr int PASSES = ES == 2 ? 1 : 2;
+  constexpr int PROWS = BM / PASSES;         // rows per pass
+  unsigned char* lds = reinterpret_cast<unsigned char*>(smem);
+  auto swz = [](int row, int chunk) { return chunk ^ (((row >> 2) & 3) * (32 / 16)); };
+  __syncthreads();  // every wave is done with the stage buffers
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p) {
+    if (PASSES == 1 || (wave >> 2) == p) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int cl = wn + j * 16 + mfma_col(lane);  // column within the tile
+        const float bv = (BIAS && n0 + cl < N) ? bf16_to_f32(bias[n0 + cl]) : 0.f;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const int rl = wm + i * 16 + mfma_row(lane, 0) - p * PROWS;  // first of 4 rows
+          if (ES == 2) {
+            const uint32_t p01 = (uint32_t)f32_to_bf16(acc[i][j][0] + bv) |
+                                 ((uint32_t)f32_to_bf16(acc[i][j][1] + bv) << 16);
+            const uint32_t p23 = (uint32_t)f32_to_bf16(acc[i][j][2] + bv) |
+                                 ((uint32_t)f32_to_bf16(acc[i][j][3] + bv) << 16);
+            const bool odd = lane & 1;
+            const uint32_t give = odd ? p01 : p23;
+            // quad_perm [1,0,3,2]: lane l receives lane l ^ 1
+            const uint32_t got = (uint32_t)__builtin_amdgcn_mov_dpp((int)give, 0xB1, 0xF, 0xF, false);
+            // even lane: rows 0, 1 of columns (cl, cl + 1); odd lane: rows 2, 3
+            // of columns (cl - 1, cl)
+            const uint32_t w0 = odd ? ((got & 0xFFFFu) | (p23 << 16)) : ((p01 & 0xFFFFu) | (got << 16));
+            const uint32_t w1 = odd ? ((got >> 16) | (p23 & 0xFFFF0000u)) : ((p01 >> 16) | (got & 0xFFFF0000u));
+            const int c0 = cl & ~1, r0 = rl + (odd ? 2 : 0);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const int row = r0 + h;
+              const int byte = c0 * 2;
+              const int off = row * ROWB + swz(row, byte >> 4) * 16 + (byte & 15);
+              *reinterpret_cast<uint32_t*>(lds + off) = h ? w1 : w0;
+            }
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int row = rl + r;
+              const int byte = cl * 4;
+              const int off = row * ROWB + swz(row, byte >> 4) * 16 + (byte & 15);
+              *reinterpret_cast<float*>(lds + off) = acc[i][j][r] + bv;
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < PROWS * CPR; e += NT) {
+      const int row = e / CPR, ch = e % CPR;
+      const int grow = m0 + p * PROWS + row, gcol = n0 + ch * EPC;
+      if (grow < M && gcol < N) {
+        const uint4 v = *reinterpret_cast<const uint4*>(lds + row * ROWB + swz(row, ch) * 16);
+        const bool sec = gcol >= C.split;
+        OutT* cb = (sec ? C.c1 : C.c0) + (int64_t)z * C.zstride;
+        const int64_t ldc = sec ? C.ld1 : C.ld0;
+        const int cc = sec ? gcol - C.split : gcol;
+        *reinterpret_cast<uint4*>(cb + (int64_t)grow * ldc + cc) = v;
+      }
+    }
+    if (p + 1 < PASSES) __syncthreads();
+  }
+}
+
 // ROWSUM: A is m-major; the workgroups of the first column of tiles write
 // the row sums of A over their split's k-range to rowsum[z * M + m].
 template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
     Op A, Op B, Out<OutT> C, const bf16_t* __restrict__ bias, float* __restrict__ rowsum,
-    int M, int N, int K, int kps, int tm, int tn, int S) {
+    int M, int N, int K, int kps, int tm, int tn, int S, int staged) {
   using CF = Cfg<BN>;
   extern __shared__ __align__(16) bf16_t smem[];
 
@@ -243,6 +332,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
       }
   }
 
+  if (staged) {
+    store_tile_staged<OutT, BN, BIAS>(acc, C, bias, smem, M, N, m0, n0, z, wm, wn, wave, lane);
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < CF::NJ; ++j) {
     const int col = n0 + wn + j * 16 + mfma_col(lane);
@@ -279,8 +372,15 @@ hipError_t launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kp
   Op A{a, g.lda, a, g.lda, 1 << 30};
   Op B{b, g.ldb, b2, g.B2 ? g.ldb2 : g.ldb, g.B2 ? g.n_split : (1 << 30)};
   const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
+  // the staged epilogue writes whole 16-byte chunks
+  constexpr int EPC = 16 / (int)sizeof(OutT);
+  const uintptr_t al = reinterpret_cast<uintptr_t>(dst.c0) | reinterpret_cast<uintptr_t>(dst.c1);
+  const bool staged = (al & 15) == 0 && g.N % EPC == 0 && dst.ld0 % EPC == 0 &&
+                      dst.ld1 % EPC == 0 && (dst.split >= g.N || dst.split % EPC == 0) &&
+                      dst.zstride % EPC == 0;
   hipLaunchKernelGGL(kern, dim3(tm * tn * S), dim3(NT), Cfg<BN>::LDS, s, A, B, dst,
-                     static_cast<const bf16_t*>(g.bias), rowsum, g.M, g.N, g.K, kps, tm, tn, S);
+                     static_cast<const bf16_t*>(g.bias), rowsum, g.M, g.N, g.K, kps, tm, tn, S,
+                     staged ? 1 : 0);
   return hipGetLastError();
 }
 

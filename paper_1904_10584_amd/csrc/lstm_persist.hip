@@ -1,5 +1,5 @@
-// Persistent LSTM layer kernels: one cooperative launch runs every time step
-// of one layer, forward or backward.
+// Persistent LSTM layer kernels: one launch, whose grid fits on the device at
+// once, runs every time step of one layer, forward or backward.
 //
 // Work split as in the single-step kernels: a workgroup owns 16 hidden units
 // and 64 sequences, and its four waves split the recurrent product's k-range
@@ -16,7 +16,8 @@
 // reading, it waits until the counter reaches (number of unit slices) x
 // (steps the block has done).  The wait is bounded: past ~0.5 s it records an
 // error flag and carries on, so every wave always reaches the end of the
-// kernel.  The launch is cooperative, so all workgroups are resident.
+// kernel.  The grid is sized to fit on the device (occupancy x CUs), so on
+// an otherwise idle device all workgroups are resident (see resident_launch).
 #include "am_device.h"
 #include "am_internal.h"
 
@@ -393,8 +394,7 @@ hipError_t coop(K kernel, dim3 grid, void** args, hipStream_t s, bool* used, int
     return hipSuccess;
   }
   *used = true;
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kernel), grid, dim3(threads), args,
-                                    0, s);
+  return resident_launch(reinterpret_cast<const void*>(kernel), grid, dim3(threads), args, 0, s);
 }
 
 template <typename T>

@@ -505,7 +505,7 @@ hipError_t coop(K kernel, int blocks, int threads, size_t lds, void** args, hipS
     return hipSuccess;
   }
   *used = true;
-  return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(threads), args, (unsigned)lds, s);
+  return resident_launch(fn, dim3(blocks), dim3(threads), args, lds, s);
 }
 
 // Shapes covered: bf16 (the resident slices are sized for it), RB = 16 or

@@ -1,6 +1,8 @@
 // Elementwise and data-movement kernels of the training step: the SGD update
 // with its bf16 copy, fp32 -> bf16 casts, the recurrent-weight transpose used
 // by BPTT, bias-gradient column sums and the final-state gather.
+#include <cstdlib>
+
 #include "am_device.h"
 #include "am_internal.h"
 
@@ -205,6 +207,16 @@ hipError_t gather_state(const GatherState& a, int b0, int nb, hipStream_t s) {
   if (a.h_bf16) hipLaunchKernelGGL(gather_state_kernel<bf16_t>, dim3(nb), dim3(256), 0, s, a, b0);
   else hipLaunchKernelGGL(gather_state_kernel<float>, dim3(nb), dim3(256), 0, s, a, b0);
   return hipGetLastError();
+}
+
+hipError_t resident_launch(const void* fn, dim3 grid, dim3 block, void** args, size_t lds,
+                           hipStream_t s) {
+  static const bool cooperative = [] {
+    const char* v = getenv("AM_COOPERATIVE");
+    return v && v[0] == '1';
+  }();
+  if (cooperative) return hipLaunchCooperativeKernel(fn, grid, block, args, (unsigned)lds, s);
+  return hipLaunchKernel(fn, grid, block, args, lds, s);
 }
 
 }  // namespace am
