@@ -22,6 +22,9 @@ What it computes, in the order the training step runs it
   matching decode, and the aggregate of several workers' sparse updates.
 * ``bmuf``     -- the BMUF-NBM global step that ends a block of local SGD
   (§VI-B, eqs. (1)-(5)).
+* ``features`` -- the student's input frames (three 10 ms frames stacked at a
+  30 ms advance, causal mean subtraction, global normalisation) and the
+  targets delayed by the model's look-ahead (§II-B).
 
 Floating point: the model, loss and their gradients are computed in fp64;
 the quantiser and SGD use the exact fp32 operation order that the method
@@ -37,6 +40,8 @@ from .soft_ce import sparse_soft_ce
 from .sgd import sgd_apply
 from .gtc import grad_threshold_encode, grad_threshold_decode, grad_threshold_decode_multi
 from .bmuf import bmuf_block_update, bmuf_zeta
+from .features import (lfr_frames, lfr_stack, causal_mean_subtract, global_mvn, lfr_features,
+                       delay_targets)
 
 __all__ = [
     "ModelDims", "param_count", "param_offsets", "unpack_params",
@@ -45,4 +50,6 @@ __all__ = [
     "sparse_soft_ce", "sgd_apply",
     "grad_threshold_encode", "grad_threshold_decode", "grad_threshold_decode_multi",
     "bmuf_block_update", "bmuf_zeta",
+    "lfr_frames", "lfr_stack", "causal_mean_subtract", "global_mvn", "lfr_features",
+    "delay_targets",
 ]

@@ -200,3 +200,36 @@ def test_decode_multi_pins_reject(old, new):
         assert failures > 0, (old, new)
     finally:
         oracle.grad_threshold_decode_multi = saved
+
+
+# ---- input features and delayed targets ---------------------------------------
+
+@pytest.mark.parametrize("old,new", [
+    ("out[t, k * D:(k + 1) * D] = raw[offset + skip * t + k]",
+     "out[t, k * D:(k + 1) * D] = raw[offset + skip * t + (stack - 1 - k)]"),      # newest frame first
+    ("        run = run + y[t]\n        z[t] = y[t] - run / (t + 1)",
+     "        z[t] = y[t] - run / max(t, 1)\n        run = run + y[t]"),           # mean of the past only
+    ("                src = int(offs[t - delay]) + b", "                src = int(offs[t - delay + 1]) + b"),  # off by one
+    ("    return max(0, (U - offset - stack) // skip + 1)", "    return max(0, (U - offset + skip - 1) // skip)"),  # partial stacks
+])
+def test_feature_pins_reject(old, new):
+    import tests.test_oracle_features as pins
+    mod = _mutant("features.py", old, new)
+    saved = {k: getattr(oracle, k) for k in ("lfr_stack", "lfr_frames", "causal_mean_subtract", "delay_targets")}
+    for k in saved:
+        setattr(oracle, k, getattr(mod, k))
+    try:
+        failures = 0
+        calls = [lambda o=o: pins.test_stacked_layout(o) for o in (0, 1, 2)]
+        calls += [lambda a=a: pins.test_frame_counts(*a) for a in ((5, 2, 1), (4, 2, 0), (2, 0, 0))]
+        calls += [pins.test_causal_mean_closed_forms]
+        calls += [lambda l=l, d=d: pins.test_delayed_targets(l, d) for l in (None, [9, 7, 7, 3, 2, 0]) for d in (1, 3)]
+        for call in calls:
+            try:
+                call()
+            except (AssertionError, IndexError, ValueError):
+                failures += 1
+        assert failures > 0, (old, new)
+    finally:
+        for k, v in saved.items():
+            setattr(oracle, k, v)
