@@ -167,6 +167,47 @@ am_status grad_threshold_decode(const uint32_t* words, const int64_t* count, int
                                 float tau, int64_t n, float* dense, int32_t accumulate,
                                 void* stream);
 
+/* ---- student inputs ------------------------------------------------------ */
+
+/* Stacked frames of an utterance of raw_frames 10 ms frames: the number of
+ * complete stacks of `stack` frames at a `skip` advance from frame `offset`
+ * (0 <= offset < skip), i.e. max(0, (raw_frames - offset - stack) / skip + 1);
+ * -1 for invalid arguments.  Host only. */
+int32_t am_lfr_frames(int32_t raw_frames, int32_t stack, int32_t skip, int32_t offset);
+
+/* The student's input frames (§II-B: 64-dim log mel energies every 10 ms,
+ * stacked three at a time and sub-sampled to a 30 ms advance at one of three
+ * offsets, a causal mean estimate subtracted, then global mean and variance
+ * normalisation).  For utterance b with T_b = am_lfr_frames(raw_lengths[b],
+ * stack, skip, offset) stacked frames, frame t (t < T_b) is
+ *   y_t = [F(offset + skip t), ..., F(offset + skip t + stack - 1)]  (oldest first)
+ *   z_t = y_t - (y_0 + ... + y_t) / (t + 1)
+ *   out_t = (z_t - mean) / std          (per dimension)
+ * evaluated in fp64 in this order without fused multiply-adds and rounded
+ * once to fp32 (then to bf16 if x_dtype is AM_BF16).
+ *   raw_lengths [host] [B] raw frames per utterance (<= 65535), in an order
+ *               whose T_b are non-increasing; B <= 1024
+ *   raw         [sum raw_lengths][raw_dim] fp32, utterance after utterance
+ *   mean, std   [stack * raw_dim] fp32 (std must be non-zero)
+ *   x           packed time-major model input [N][stack * raw_dim] of
+ *               x_dtype: frame (t, b) is row off_t + b as in lstm_am_forward
+ *               with lengths T_b; N = sum T_b.                              */
+am_status lfr_features(int32_t B, const int32_t* raw_lengths, const float* raw, int32_t raw_dim,
+                       int32_t stack, int32_t skip, int32_t offset, const float* mean,
+                       const float* std, void* x, int32_t x_dtype, void* stream);
+
+/* Targets for a model with a `delay`-frame look-ahead (§II-B: three frames):
+ * packed row (t, b) takes the target of row (t - delay, b) of the same
+ * sequence; rows with t < delay get idx -1, prob 0 and mask 0, every other
+ * row mask 1.  The mask goes to sparse_soft_ce.  T, B, lengths as in
+ * lstm_am_forward (B <= 1024, T <= 65535); idx, prob [N][K] in; idx_out,
+ * prob_out [N][K] and mask_out [N] out (must not alias the inputs).  A caller
+ * that scores the last `delay` targets of an utterance extends its input by
+ * `delay` frames.                                                           */
+am_status delay_targets(int32_t T, int32_t B, const int32_t* lengths, int32_t K, int32_t delay,
+                        const int32_t* idx, const float* prob, int32_t* idx_out, float* prob_out,
+                        uint8_t* mask_out, void* stream);
+
 /* Aggregate of the sparse updates of several workers (§VI-A: each worker
  * receives every other worker's sparse update and aggregates them).  Stream
  * s is row s of `words` [streams][capacity] (for example the result of a

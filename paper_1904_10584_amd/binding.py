@@ -69,6 +69,9 @@ _PROTOS = {
     "am_decode_multi_workspace_bytes": (_I64, [_I32, _I64]),
     "grad_threshold_decode_multi": (_I32, [_I32, _P, _I64, _P, _F32, _I64, _P, _I32, _P, _I64, _P]),
     "bmuf_block_update": (_I32, [_I64, _I32, _I32, _P, _I64, _P, _P, _F32, _F32, _F32, _P, _P, _P]),
+    "am_lfr_frames": (_I32, [_I32, _I32, _I32, _I32]),
+    "lfr_features": (_I32, [_I32, _P, _P, _I32, _I32, _I32, _I32, _P, _P, _P, _I32, _P]),
+    "delay_targets": (_I32, [_I32, _I32, _P, _I32, _I32, _P, _P, _P, _P, _P, _P]),
     "am_cast_f32_to_bf16": (_I32, [_I64, _P, _P, _P]),
     "am_workspace_check": (_I32, [_P, _I64, _P]),
     "am_profile_begin": (_I32, [ctypes.c_uint32]),
@@ -246,6 +249,28 @@ def bmuf_block_update(models, workers, global_model, delta, eta, eta_next, zeta,
         float(eta), float(eta_next), float(zeta),
         _dev(local_master, "local_master", torch.float32),
         _dev(local_bf16, "local_bf16", torch.bfloat16), _stream(stream)))
+
+
+def lfr_frames(raw_frames, stack=3, skip=3, offset=0) -> int:
+    return int(lib().am_lfr_frames(raw_frames, stack, skip, offset))
+
+
+def lfr_features(raw_lengths, raw, mean, std, x, stack=3, skip=3, offset=0, stream=None):
+    """raw: [sum raw_lengths][raw_dim] fp32 GPU tensor; x: packed model input."""
+    arr, lp = _host_i32(raw_lengths)
+    dt = BF16 if x.dtype == torch.bfloat16 else F32
+    _check(lib().lfr_features(
+        len(raw_lengths), lp, _dev(raw, "raw", torch.float32), raw.shape[1], stack, skip, offset,
+        _dev(mean, "mean", torch.float32), _dev(std, "std", torch.float32), _dev(x, "x"), dt,
+        _stream(stream)))
+
+
+def delay_targets(T, B, idx, prob, idx_out, prob_out, mask_out, delay, lengths=None, stream=None):
+    arr, lp = _host_i32(lengths)
+    _check(lib().delay_targets(
+        T, B, lp, idx.shape[1], delay, _dev(idx, "idx", torch.int32), _dev(prob, "prob", torch.float32),
+        _dev(idx_out, "idx_out", torch.int32), _dev(prob_out, "prob_out", torch.float32),
+        _dev(mask_out, "mask_out", torch.uint8), _stream(stream)))
 
 
 def sgd_apply(master, update, lr, weights_bf16=None, stream=None):

@@ -156,6 +156,25 @@ hipError_t gtc_decode_multi(int streams, const uint32_t* words, int64_t capacity
                             const int64_t* counts, float tau, int64_t n, float* dense,
                             bool accumulate, int32_t* ws_start, hipStream_t s);
 
+// Stacked low-frame-rate input frames (see lfr_features in the C ABI).
+struct LfrArgs {
+  int B, raw_dim, stack, skip, offset;
+  uint16_t U[1024];    // raw frames per utterance
+  const float* raw;    // [sum U][raw_dim], utterance after utterance
+  const float* mean;   // [stack * raw_dim]
+  const float* std;    // [stack * raw_dim]
+  void* x;             // packed [N][stack * raw_dim], model dtype
+};
+hipError_t lfr_features(const LfrArgs& a, bool bf16, hipStream_t s);
+// Targets of packed rows delayed by `delay` frames within each sequence.
+struct DelayArgs {
+  int T, B, K, delay;
+  uint16_t len[1024];
+  const int32_t* idx; const float* prob;
+  int32_t* idx_out; float* prob_out; uint8_t* mask_out;
+};
+hipError_t delay_targets(const DelayArgs& a, hipStream_t s);
+
 // BMUF-NBM global step (count addends of stride elements, divided by workers).
 hipError_t bmuf_update(int64_t n, int count, int workers, const float* models, int64_t stride,
                        float* wg, float* delta, float eta, float eta_next, float zeta,

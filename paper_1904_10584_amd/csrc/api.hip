@@ -451,6 +451,66 @@ am_status bmuf_block_update(int64_t n, int32_t count, int32_t workers, const flo
                    "bmuf_block_update");
 }
 
+int32_t am_lfr_frames(int32_t raw_frames, int32_t stack, int32_t skip, int32_t offset) {
+  if (raw_frames < 0 || stack < 1 || skip < 1 || offset < 0 || offset >= skip) return -1;
+  const int32_t r = raw_frames - offset - stack;
+  return r < 0 ? 0 : r / skip + 1;
+}
+
+am_status lfr_features(int32_t B, const int32_t* raw_lengths, const float* raw, int32_t raw_dim,
+                       int32_t stack, int32_t skip, int32_t offset, const float* mean,
+                       const float* std, void* x, int32_t x_dtype, void* stream) {
+  if (B < 0 || B > 1024) return fail(AM_EUNSUPPORTED, "B must be in [0, 1024]");
+  if (raw_dim < 1 || stack < 1 || skip < 1 || offset < 0 || offset >= skip)
+    return fail(AM_EINVAL, "need raw_dim, stack, skip >= 1 and 0 <= offset < skip");
+  if ((int64_t)stack * raw_dim > 4096) return fail(AM_EUNSUPPORTED, "stack * raw_dim > 4096");
+  if (x_dtype != AM_F32 && x_dtype != AM_BF16) return fail(AM_EINVAL, "unknown x dtype");
+  if (B > 0 && !raw_lengths) return fail(AM_EINVAL, "raw_lengths is NULL");
+  am::LfrArgs a;
+  memset(&a, 0, sizeof a);
+  a.B = B; a.raw_dim = raw_dim; a.stack = stack; a.skip = skip; a.offset = offset;
+  int64_t frames = 0, raws = 0;
+  int32_t prev = 0;
+  for (int b = 0; b < B; ++b) {
+    if (raw_lengths[b] < 0 || raw_lengths[b] > 65535)
+      return fail(AM_EUNSUPPORTED, "raw_lengths[%d] = %d outside [0, 65535]", b, raw_lengths[b]);
+    const int32_t T = am_lfr_frames(raw_lengths[b], stack, skip, offset);
+    if (b > 0 && T > prev)
+      return fail(AM_EINVAL, "stacked lengths must be non-increasing (utterance %d)", b);
+    prev = T;
+    frames += T;
+    raws += raw_lengths[b];
+    a.U[b] = (uint16_t)raw_lengths[b];
+  }
+  if (raws > 0 && !raw) return fail(AM_EINVAL, "raw is NULL");
+  if (frames > 0 && (!x || !mean || !std)) return fail(AM_EINVAL, "NULL x, mean or std");
+  a.raw = raw; a.mean = mean; a.std = std; a.x = x;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const double bytes = (double)frames * stack * raw_dim * (4 + (x_dtype == AM_BF16 ? 2 : 4));
+  Timed tm(AM_K_MISC, s, 0.0, bytes);
+  return hip_check(am::lfr_features(a, x_dtype == AM_BF16, s), "lfr_features");
+}
+
+am_status delay_targets(int32_t T, int32_t B, const int32_t* lengths, int32_t K, int32_t delay,
+                        const int32_t* idx, const float* prob, int32_t* idx_out, float* prob_out,
+                        uint8_t* mask_out, void* stream) {
+  if (T > 65535) return fail(AM_EUNSUPPORTED, "T > 65535");
+  if (K < 0 || delay < 0) return fail(AM_EINVAL, "need K >= 0 and delay >= 0");
+  Schedule sc;
+  AM_TRY(make_schedule(T, B, lengths, sc));
+  if (sc.N > 0 && (!mask_out || (K > 0 && (!idx || !prob || !idx_out || !prob_out))))
+    return fail(AM_EINVAL, "NULL pointer");
+  am::DelayArgs a;
+  memset(&a, 0, sizeof a);
+  if (B > 1024) return fail(AM_EUNSUPPORTED, "B > 1024");
+  a.T = T; a.B = B; a.K = K; a.delay = delay;
+  for (int b = 0; b < B; ++b) a.len[b] = (uint16_t)sc.lens[b];
+  a.idx = idx; a.prob = prob; a.idx_out = idx_out; a.prob_out = prob_out; a.mask_out = mask_out;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Timed tm(AM_K_MISC, s, 0.0, (double)sc.N * (16.0 * K + 1));
+  return hip_check(am::delay_targets(a, s), "delay_targets");
+}
+
 am_status sparse_soft_ce(int64_t N, int32_t C, int32_t K, const float* logits, const int32_t* idx,
                          const float* prob, const uint8_t* mask, int32_t reduction, float* loss,
                          void* dlogits, int32_t dlogits_dtype, void* ws, int64_t ws_bytes,

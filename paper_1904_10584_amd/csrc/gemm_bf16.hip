@@ -375,9 +375,12 @@ hipError_t launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kp
   // the staged epilogue writes whole 16-byte chunks
   constexpr int EPC = 16 / (int)sizeof(OutT);
   const uintptr_t al = reinterpret_cast<uintptr_t>(dst.c0) | reinterpret_cast<uintptr_t>(dst.c1);
+  // (split-K fp32 partials keep the direct stores: their tiles have long
+  // k-loops, 64-byte store segments, and two LDS passes cost more than
+  // they save)
   const bool staged = (al & 15) == 0 && g.N % EPC == 0 && dst.ld0 % EPC == 0 &&
                       dst.ld1 % EPC == 0 && (dst.split >= g.N || dst.split % EPC == 0) &&
-                      dst.zstride % EPC == 0;
+                      dst.zstride % EPC == 0 && (sizeof(OutT) == 2 || S == 1);
   hipLaunchKernelGGL(kern, dim3(tm * tn * S), dim3(NT), Cfg<BN>::LDS, s, A, B, dst,
                      static_cast<const bf16_t*>(g.bias), rowsum, g.M, g.N, g.K, kps, tm, tn, S,
                      staged ? 1 : 0);

@@ -17,14 +17,18 @@ of them): local models that drifted from the global model over a block of
 local SGD (the global model plus N(0, spread^2) noise per worker), and
 per-worker gradients of the scale of the training step's (N(0, scale^2)).
 
+Stand-in for raw 10 ms log mel energies (before stacking, §II-B): per
+utterance a per-dimension level N(2, 3^2) plus a slow random-walk drift
+(so that the causal mean matters) plus N(0, 1) frame noise.
+
 Seeds: weights 0, features 1, targets 2, lengths 3, one-hot frame choice 4,
-worker models 5, worker gradients 6.
+worker models 5, worker gradients 6, raw log mel frames 7.
 """
 
 import numpy as np
 
 SEED_WEIGHTS, SEED_FEATURES, SEED_TARGETS, SEED_LENGTHS, SEED_ONEHOT = 0, 1, 2, 3, 4
-SEED_WORKER_MODELS, SEED_WORKER_GRADS = 5, 6
+SEED_WORKER_MODELS, SEED_WORKER_GRADS, SEED_RAW = 5, 6, 7
 
 # Workload shapes.  dtype "f32": fp32 throughout; "bf16": bf16 weights and
 # activations with fp32 master weights.
@@ -103,3 +107,16 @@ def worker_gradients(n, workers, scale, seed=SEED_WORKER_GRADS):
     """[workers][n] fp32 gradients, i.i.d. N(0, scale^2)."""
     rng = np.random.default_rng(seed)
     return (rng.standard_normal((workers, n), dtype=np.float32) * np.float32(scale))
+
+
+def raw_logmel(raw_lengths, dim=64, seed=SEED_RAW):
+    """[sum raw_lengths][dim] fp32, utterance after utterance."""
+    rng = np.random.default_rng(seed)
+    parts = []
+    for U in raw_lengths:
+        level = rng.normal(2.0, 3.0, dim)
+        drift = np.cumsum(rng.normal(0.0, 0.05, (int(U), dim)), axis=0)
+        parts.append(level[None, :] + drift + rng.standard_normal((int(U), dim)))
+    if not parts:
+        return np.zeros((0, dim), np.float32)
+    return np.concatenate(parts).astype(np.float32)
