@@ -37,7 +37,7 @@ def parse():
     ap.add_argument("--workload", default="paper-5x768")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-worker-kernels", action="store_true",
-                    help="skip timing the multi-worker pieces (BMUF step, 8-stream aggregate)")
+                    help="skip timing the side kernels (BMUF step, 8-stream aggregate, input features, target delay)")
     ap.add_argument("--cpu-chunks", type=int, default=0,
                     help="chunks the CPU oracle runs forward/backward on (0 = the whole batch)")
     return ap.parse_args()
@@ -172,6 +172,39 @@ def worker_kernels(am, n, reps):
     return out
 
 
+def input_kernels(am, synth, w, N, reps):
+    """The student's input pieces for one batch of the workload (outside the
+    timed step): stacked 30 ms features from raw 10 ms log mel frames of
+    every chunk (stack 3, skip 3, causal mean, global normalisation) and the
+    targets delayed by a three-frame look-ahead."""
+    import numpy as np
+    import torch
+    B, T, K = w["B"], w["T"], w["K"]
+    U = np.full(B, 3 * T + 2, np.int32)
+    raw = torch.from_numpy(synth.raw_logmel(U)).cuda()
+    mean = torch.zeros(3 * 64, device="cuda")
+    std = torch.ones(3 * 64, device="cuda")
+    x = torch.empty((T * B, 3 * 64), dtype=torch.bfloat16, device="cuda")
+    idx = torch.zeros((T * B, K), dtype=torch.int32, device="cuda")
+    prob = torch.zeros((T * B, K), dtype=torch.float32, device="cuda")
+    io, po = torch.empty_like(idx), torch.empty_like(prob)
+    mo = torch.empty((T * B,), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    out = {}
+    am.profile_begin([am.K_MISC])
+    for _ in range(reps):
+        am.lfr_features(U, raw, mean, std, x)
+    am.profile_end()
+    out["lfr_features"] = dict(_hbm_entry(am.profile_get(am.K_MISC), reps), frames=T * B,
+                               raw_frames=int(U.sum()))
+    am.profile_begin([am.K_MISC])
+    for _ in range(reps):
+        am.delay_targets(T, B, idx, prob, io, po, mo, 3)
+    am.profile_end()
+    out["delay_targets"] = dict(_hbm_entry(am.profile_get(am.K_MISC), reps), rows=T * B, k=K)
+    return out
+
+
 def cpu_baseline(wl, synth, chunks):
     """The oracle, as it stands, on a bounded sample: forward, CE and BPTT on
     `chunks` chunks of the batch, plus encode, decode and SGD of the whole
@@ -299,6 +332,8 @@ def main():
     }
     if not args.no_worker_kernels:
         out["worker_kernels"] = worker_kernels(am, st.n, reps=10)
+        if lengths is None:
+            out["input_kernels"] = input_kernels(am, synth, w, N, reps=10)
     if not args.no_cpu_baseline and args.workload in ("paper-5x768", "tiny-2x64", "wide-5x1536"):
         out["cpu_baseline"] = cpu_baseline(args.workload, synth, args.cpu_chunks)
     print(json.dumps(out), flush=True)
