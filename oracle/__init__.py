@@ -25,6 +25,9 @@ What it computes, in the order the training step runs it
 * ``features`` -- the student's input frames (three 10 ms frames stacked at a
   30 ms advance, causal mean subtraction, global normalisation) and the
   targets delayed by the model's look-ahead (§II-B).
+* ``teacher``  -- target generation: the bidirectional LSTM teacher's logits,
+  the k best logits per frame and the posterior rebuilt from them (§V-A,
+  §V-C, §VII).
 
 Floating point: the model, loss and their gradients are computed in fp64;
 the quantiser and SGD use the exact fp32 operation order that the method
@@ -42,6 +45,8 @@ from .gtc import grad_threshold_encode, grad_threshold_decode, grad_threshold_de
 from .bmuf import bmuf_block_update, bmuf_zeta
 from .features import (lfr_frames, lfr_stack, causal_mean_subtract, global_mvn, lfr_features,
                        delay_targets)
+from .teacher import (TeacherDims, teacher_param_count, teacher_param_offsets, teacher_forward,
+                      topk_logits, kbest_posteriors)
 
 __all__ = [
     "ModelDims", "param_count", "param_offsets", "unpack_params",
@@ -52,4 +57,6 @@ __all__ = [
     "bmuf_block_update", "bmuf_zeta",
     "lfr_frames", "lfr_stack", "causal_mean_subtract", "global_mvn", "lfr_features",
     "delay_targets",
+    "TeacherDims", "teacher_param_count", "teacher_param_offsets", "teacher_forward",
+    "topk_logits", "kbest_posteriors",
 ]

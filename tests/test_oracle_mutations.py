@@ -233,3 +233,33 @@ def test_feature_pins_reject(old, new):
     finally:
         for k, v in saved.items():
             setattr(oracle, k, v)
+
+
+# ---- teacher -------------------------------------------------------------------
+
+@pytest.mark.parametrize("old,new", [
+    ("out[r, H:] = _lstm_sequence(xs[::-1], dirs[1], H)[::-1]",
+     "out[r, H:] = _lstm_sequence(xs[::-1], dirs[1], H)"),              # not reversed back
+    ("out[r, H:] = _lstm_sequence(xs[::-1], dirs[1], H)[::-1]",
+     "out[r, H:] = _lstm_sequence(xs, dirs[1], H)"),                    # backward runs forward
+    ("order = np.argsort(-z, axis=1, kind=\"stable\")[:, :k]",
+     "order = np.argsort(z, axis=1, kind=\"stable\")[:, ::-1][:, :k]"),  # ties: higher index first
+])
+def test_teacher_pins_reject(old, new):
+    import tests.test_oracle_teacher as pins
+    mod = _mutant("teacher.py", old, new)
+    saved = (oracle.teacher_forward, oracle.topk_logits)
+    oracle.teacher_forward, oracle.topk_logits = mod.teacher_forward, mod.topk_logits
+    try:
+        failures = 0
+        for call in (lambda: pins.test_matches_torch_bidirectional_lstm(None),
+                     lambda: pins.test_matches_torch_bidirectional_lstm([7, 7, 5, 2, 1]),
+                     pins.test_time_reversal_swaps_the_directions,
+                     pins.test_topk_against_repeated_maximum):
+            try:
+                call()
+            except AssertionError:
+                failures += 1
+        assert failures > 0, (old, new)
+    finally:
+        oracle.teacher_forward, oracle.topk_logits = saved
