@@ -208,6 +208,39 @@ am_status delay_targets(int32_t T, int32_t B, const int32_t* lengths, int32_t K,
                         const int32_t* idx, const float* prob, int32_t* idx_out, float* prob_out,
                         uint8_t* mask_out, void* stream);
 
+/* ---- teacher target generation ------------------------------------------ */
+
+/* The teacher (§V-A, §VII): `layers` bidirectional LSTM layers of `hidden`
+ * cells per direction over input_dim-dim frames, then a senone layer over
+ * both directions' outputs.  Each direction is the student's cell; the
+ * backward direction runs over each sequence from its last frame to its
+ * first, from a zero state; a layer's output is [h_forward, h_backward].
+ * Flat parameters: per layer, forward Wx [4H][D_l], Wh [4H][H], b [4H], then
+ * the backward direction's (D_0 = input_dim, D_l = 2H); then Wo [C][2H],
+ * bo [C].  The offsets query writes 6L + 2 offsets in that order. */
+int64_t am_teacher_param_count(const am_model* m);
+am_status am_teacher_param_offsets(const am_model* m, int64_t* offsets);
+int64_t am_teacher_workspace_bytes(const am_model* m, int32_t T, int32_t B, int64_t N);
+
+/* Teacher logits [N][C] fp32 for packed frames x (layout, lengths and dtypes
+ * as lstm_am_forward; B <= 1024, T <= 65535).  Inference only: `ws` holds
+ * scratch of this call alone.                                              */
+am_status blstm_teacher_forward(const am_model* m, const void* params, const void* x,
+                                const int32_t* lengths, int32_t T, int32_t B, float* logits,
+                                void* ws, int64_t ws_bytes, void* stream);
+
+/* The K largest logits of each row (§V-C: the teacher's targets are stored
+ * as its k best logits, k = 20), in descending order, equal values by
+ * ascending index, NaN after every number: idx [N][K] int32, val [N][K]
+ * fp32.  K <= min(C, 64), C <= 8192.                                        */
+am_status kbest_logits(int64_t N, int32_t C, int32_t K, const float* logits, int32_t* idx,
+                       float* val, void* stream);
+
+/* The posterior rebuilt from K stored logits with every missing logit at
+ * -infinity (§V-C fills them with large negative values): per row, the
+ * softmax over the K values, fp32 (prob [N][K]), for sparse_soft_ce.       */
+am_status kbest_posteriors(int64_t N, int32_t K, const float* val, float* prob, void* stream);
+
 /* Aggregate of the sparse updates of several workers (§VI-A: each worker
  * receives every other worker's sparse update and aggregates them).  Stream
  * s is row s of `words` [streams][capacity] (for example the result of a

@@ -70,6 +70,12 @@ _PROTOS = {
     "grad_threshold_decode_multi": (_I32, [_I32, _P, _I64, _P, _F32, _I64, _P, _I32, _P, _I64, _P]),
     "bmuf_block_update": (_I32, [_I64, _I32, _I32, _P, _I64, _P, _P, _F32, _F32, _F32, _P, _P, _P]),
     "am_lfr_frames": (_I32, [_I32, _I32, _I32, _I32]),
+    "am_teacher_param_count": (_I64, [_P]),
+    "am_teacher_param_offsets": (_I32, [_P, _P]),
+    "am_teacher_workspace_bytes": (_I64, [_P, _I32, _I32, _I64]),
+    "blstm_teacher_forward": (_I32, [_P, _P, _P, _P, _I32, _I32, _P, _P, _I64, _P]),
+    "kbest_logits": (_I32, [_I64, _I32, _I32, _P, _P, _P, _P]),
+    "kbest_posteriors": (_I32, [_I64, _I32, _P, _P, _P]),
     "lfr_features": (_I32, [_I32, _P, _P, _I32, _I32, _I32, _I32, _P, _P, _P, _I32, _P]),
     "delay_targets": (_I32, [_I32, _I32, _P, _I32, _I32, _P, _P, _P, _P, _P, _P]),
     "am_cast_f32_to_bf16": (_I32, [_I64, _P, _P, _P]),
@@ -271,6 +277,48 @@ def delay_targets(T, B, idx, prob, idx_out, prob_out, mask_out, delay, lengths=N
         T, B, lp, idx.shape[1], delay, _dev(idx, "idx", torch.int32), _dev(prob, "prob", torch.float32),
         _dev(idx_out, "idx_out", torch.int32), _dev(prob_out, "prob_out", torch.float32),
         _dev(mask_out, "mask_out", torch.uint8), _stream(stream)))
+
+
+def teacher_param_count(m: Model) -> int:
+    n = lib().am_teacher_param_count(ctypes.byref(m.c()))
+    if n < 0:
+        _check(-1)
+    return int(n)
+
+
+def teacher_param_offsets(m: Model):
+    out = (ctypes.c_int64 * (6 * m.layers + 2))()
+    _check(lib().am_teacher_param_offsets(ctypes.byref(m.c()), out))
+    return list(out)
+
+
+def teacher_workspace_bytes(m: Model, T, B, N) -> int:
+    n = lib().am_teacher_workspace_bytes(ctypes.byref(m.c()), T, B, N)
+    if n < 0:
+        raise AmError("invalid model or batch for workspace query")
+    return int(n)
+
+
+def blstm_teacher_forward(m: Model, params, x, T, B, logits, ws, lengths=None, stream=None):
+    dt = m.torch_dtype
+    arr, lp = _host_i32(lengths)
+    _check(lib().blstm_teacher_forward(
+        ctypes.byref(m.c()), _dev(params, "params", dt), _dev(x, "x", dt), lp, T, B,
+        _dev(logits, "logits", torch.float32), _dev(ws, "ws"), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def kbest_logits(logits, idx, val, stream=None):
+    N, C = logits.shape
+    _check(lib().kbest_logits(N, C, idx.shape[1], _dev(logits, "logits", torch.float32),
+                              _dev(idx, "idx", torch.int32), _dev(val, "val", torch.float32),
+                              _stream(stream)))
+
+
+def kbest_posteriors(val, prob, stream=None):
+    N, K = val.shape
+    _check(lib().kbest_posteriors(N, K, _dev(val, "val", torch.float32),
+                                  _dev(prob, "prob", torch.float32), _stream(stream)))
 
 
 def sgd_apply(master, update, lr, weights_bf16=None, stream=None):

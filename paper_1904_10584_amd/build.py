@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmi355am.so")
-SOURCES = ["api.hip", "gemm.hip", "gemm_bf16.hip", "lstm_step.hip", "lstm_persist.hip", "lstm_xcd.hip", "soft_ce.hip", "gtc.hip", "misc.hip", "bmuf.hip", "features.hip"]
+SOURCES = ["api.hip", "gemm.hip", "gemm_bf16.hip", "lstm_step.hip", "lstm_persist.hip", "lstm_xcd.hip", "soft_ce.hip", "gtc.hip", "misc.hip", "bmuf.hip", "features.hip", "teacher.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

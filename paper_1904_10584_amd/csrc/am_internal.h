@@ -175,6 +175,29 @@ struct DelayArgs {
 };
 hipError_t delay_targets(const DelayArgs& a, hipStream_t s);
 
+// Teacher target generation.
+struct GatherRows {
+  const void* src; int64_t src_ld;
+  void* dst; int64_t dst_ld; int64_t dst_col;
+  int width;             // elements per row (a multiple of 16 bytes)
+  int64_t N;             // rows
+  int T;                 // time steps of the schedule
+  const int64_t* offs;   // [T + 1] packed row offsets (device)
+  const int32_t* lens;   // [B] sequence lengths (device)
+  int reverse;           // row (t, b) takes row (len_b - 1 - t, b)
+};
+hipError_t gather_rows(const GatherRows& a, bool bf16, hipStream_t s);
+struct SchedTables {
+  int T, B;
+  uint16_t len[1024];
+  int64_t* offs;  // [T + 1] out
+  int32_t* lens;  // [B] out
+};
+hipError_t schedule_tables(const SchedTables& a, hipStream_t s);
+hipError_t topk_rows(int64_t N, int C, int K, const float* z, int32_t* idx, float* val,
+                     hipStream_t s);
+hipError_t kbest_posteriors(int64_t N, int K, const float* val, float* prob, hipStream_t s);
+
 // BMUF-NBM global step (count addends of stride elements, divided by workers).
 hipError_t bmuf_update(int64_t n, int count, int workers, const float* models, int64_t stride,
                        float* wg, float* delta, float eta, float eta_next, float zeta,

@@ -258,6 +258,85 @@ WsLayout ws_layout(const am_model* m, int64_t B, int64_t N) {
   return w;
 }
 
+// One layer's recurrence, forward in time, over the packed rows of a
+// schedule: the XCD-local persistent kernel where it covers the shape, else
+// the device-scope persistent kernel, else one launch per time step.
+struct FwdLayer {
+  const void* P;      // [N][4H] input projections + bias
+  const void* Wh;     // [4H][H]
+  const void* h0;     // [B][H] activation type, or null (zero)
+  const float* c0;    // [B][H]
+  void* H; void* Hs; float* C; void* G;  // outputs [N][H], [N][H], [N][H], [N][4H]
+  void* sync;         // the workspace's sync region
+};
+
+am_status forward_recurrence(const FwdLayer& f, const Schedule& sc, bool bf, int64_t H,
+                             hipStream_t s) {
+  const int64_t e = bf ? 2 : 4, G = 4 * H;
+  const int T = sc.T, B = sc.B;
+  if (sc.N > 0 && persistent_enabled()) {
+    am::PersistFwd pa;
+    pa.P = f.P;
+    pa.Wh = f.Wh;
+    pa.h0 = f.h0;
+    pa.c0 = f.c0;
+    pa.H = f.H;
+    pa.Hs = f.Hs;
+    pa.C = f.C;
+    pa.G = f.G;
+    pa.counters = static_cast<unsigned*>(f.sync);
+    pa.err = static_cast<int*>(f.sync) + SYNC_STICKY_WORD;
+    pa.hidden = (int)H;
+    const am::PersistSchedule ps = persist_schedule(sc);
+    const double flops = 2.0 * sc.N * G * H;
+    const double bytes = (double)sc.N * (G * e * 2 + H * (2 * e + 4)) + (double)G * H * e;
+    bool used = false;
+    if (bf && xcd_enabled() && am::lstm_xcd_instantiated(true, (int)H, B)) {
+      AM_TRY(hip_check(am::fill_zero(static_cast<float*>(f.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
+      Timed tm(AM_K_LSTM_FWD, s, flops, bytes);
+      AM_TRY(hip_check(am::lstm_fwd_xcd_launch(pa, ps, xcd_sync(f.sync), s, &used),
+                       "lstm forward layer (xcd)"));
+      if (!used) tm.cancel();
+    }
+    if (!used && device_persistent_enabled() && am::lstm_persistent_fits(true, (int)H, B, bf, T)) {
+      AM_TRY(hip_check(am::fill_zero(static_cast<float*>(f.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
+      Timed tm(AM_K_LSTM_FWD, s, flops, bytes);
+      AM_TRY(hip_check(am::lstm_fwd_persistent(pa, ps, bf, s, &used), "lstm forward layer"));
+      if (!used) tm.cancel();
+    }
+    if (used) return AM_OK;
+  }
+  const char* Hl = static_cast<const char*>(f.H);
+  const float* Cl = f.C;
+  for (int t = 0; t < T; ++t) {
+    const int64_t nb = sc.counts[t];
+    if (nb == 0) break;
+    const int64_t o = sc.offs[t];
+    am::LstmFwdStep a;
+    a.P = static_cast<const char*>(f.P) + o * G * e;
+    a.Wh = f.Wh;
+    if (t == 0) {
+      a.hprev = f.h0;
+      a.cprev = f.c0;
+    } else {
+      a.hprev = Hl + sc.offs[t - 1] * H * e;
+      a.cprev = Cl + sc.offs[t - 1] * H;
+    }
+    a.H = static_cast<char*>(f.H) + o * H * e;
+    a.Hs = static_cast<char*>(f.Hs) + o * H * e;
+    a.C = f.C + o * H;
+    a.G = static_cast<char*>(f.G) + o * G * e;
+    a.nb = (int)nb;
+    a.hidden = (int)H;
+    a.bf16 = bf;
+    const double bytes = (double)(nb * H + G * H + nb * G) * e + nb * H * 4.0 +
+                         (double)nb * (H * (2 * e + 4) + G * e);
+    Timed tm(AM_K_LSTM_FWD, s, 2.0 * nb * G * H, bytes);
+    AM_TRY(hip_check(am::lstm_fwd_step(a, s), "lstm forward step"));
+  }
+  return AM_OK;
+}
+
 template <typename P> P* at(void* base, int64_t off) {
   return reinterpret_cast<P*>(static_cast<char*>(base) + off);
 }
@@ -301,6 +380,57 @@ am::GemmArgs mk_wgrad(const void* A, int64_t lda, const void* B, int64_t ldb, in
   g.M = M; g.N = nB + (B2 ? nB2 : 0); g.K = K; g.bf16 = bf16;
   g.ws = ws; g.ws_floats = ws_floats;
   return g;
+}
+
+// Teacher: per layer, forward Wx [4H][D_l], Wh [4H][H], b [4H], then the
+// backward direction's; D_0 = input_dim, D_l = 2H; then Wo [C][2H], bo [C].
+struct TeacherOffsets {
+  std::vector<int64_t> wx, wh, b;  // [layer * 2 + direction]
+  int64_t wo, bo, n;
+};
+
+TeacherOffsets teacher_layout(const am_model* m) {
+  TeacherOffsets o;
+  const int64_t H = m->hidden, G = 4 * H;
+  int64_t pos = 0;
+  for (int l = 0; l < m->layers; ++l) {
+    const int64_t D = l == 0 ? m->input_dim : 2 * H;
+    for (int d = 0; d < 2; ++d) {
+      o.wx.push_back(pos); pos += G * D;
+      o.wh.push_back(pos); pos += G * H;
+      o.b.push_back(pos); pos += G;
+    }
+  }
+  o.wo = pos; pos += (int64_t)m->classes * 2 * H;
+  o.bo = pos; pos += m->classes;
+  o.n = pos;
+  return o;
+}
+
+struct TeacherWs {
+  int64_t sync, offs, lens, cat0, cat1, rev, p, hdir, hs, c, g, c0, total;
+};
+
+TeacherWs teacher_ws_layout(const am_model* m, int64_t T, int64_t B, int64_t N) {
+  TeacherWs w;
+  const int64_t e = esz_of(m->dtype), H = m->hidden, G = 4 * H;
+  const int64_t Dmax = m->input_dim > 2 * H ? m->input_dim : 2 * H;
+  int64_t pos = 0;
+  auto take = [&](int64_t bytes) { int64_t at = pos; pos += align256(bytes); return at; };
+  w.sync = take(SYNC_BYTES);
+  w.offs = take((T + 1) * 8);
+  w.lens = take(B * 4);
+  w.cat0 = take(N * 2 * H * e);
+  w.cat1 = take(N * 2 * H * e);
+  w.rev = take(N * Dmax * e);
+  w.p = take(N * G * e);
+  w.hdir = take(N * H * e);
+  w.hs = take(N * H * e);
+  w.c = take(N * H * 4);
+  w.g = take(N * G * e);
+  w.c0 = take(B * H * 4);
+  w.total = pos;
+  return w;
 }
 
 }  // namespace
@@ -511,6 +641,128 @@ am_status delay_targets(int32_t T, int32_t B, const int32_t* lengths, int32_t K,
   return hip_check(am::delay_targets(a, s), "delay_targets");
 }
 
+int64_t am_teacher_param_count(const am_model* m) {
+  if (check_model(m) != AM_OK) return -1;
+  return teacher_layout(m).n;
+}
+
+am_status am_teacher_param_offsets(const am_model* m, int64_t* offsets) {
+  AM_TRY(check_model(m));
+  if (!offsets) return fail(AM_EINVAL, "offsets is NULL");
+  const TeacherOffsets o = teacher_layout(m);
+  for (int k = 0; k < 2 * m->layers; ++k) {
+    offsets[3 * k] = o.wx[k];
+    offsets[3 * k + 1] = o.wh[k];
+    offsets[3 * k + 2] = o.b[k];
+  }
+  offsets[6 * m->layers] = o.wo;
+  offsets[6 * m->layers + 1] = o.bo;
+  return AM_OK;
+}
+
+int64_t am_teacher_workspace_bytes(const am_model* m, int32_t T, int32_t B, int64_t N) {
+  if (check_model(m) != AM_OK || T < 0 || B < 1 || N < 0 || N > (int64_t)T * B) return -1;
+  return teacher_ws_layout(m, T, B, N).total;
+}
+
+am_status blstm_teacher_forward(const am_model* m, const void* params, const void* x,
+                                const int32_t* lengths, int32_t T, int32_t B, float* logits,
+                                void* ws, int64_t ws_bytes, void* stream) {
+  AM_TRY(check_model(m));
+  if (B > 1024 || T > 65535) return fail(AM_EUNSUPPORTED, "the teacher allows B <= 1024, T <= 65535");
+  Schedule sc;
+  AM_TRY(make_schedule(T, B, lengths, sc));
+  if (!params || !ws) return fail(AM_EINVAL, "NULL params or workspace");
+  if (sc.N > 0 && (!x || !logits)) return fail(AM_EINVAL, "NULL x or logits");
+  if (!aligned(params, 16) || !aligned(x, 16) || !aligned(logits, 16) || !aligned(ws, 256))
+    return fail(AM_EINVAL, "params, x, logits must be 16-byte and ws 256-byte aligned");
+  const TeacherWs w = teacher_ws_layout(m, T, B, sc.N);
+  if (ws_bytes < w.total)
+    return fail(AM_EWORKSPACE, "teacher forward needs %lld workspace bytes", (long long)w.total);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf = m->dtype == AM_BF16;
+  const int64_t e = esz_of(m->dtype), H = m->hidden, G = 4 * H, L = m->layers;
+  const TeacherOffsets po = teacher_layout(m);
+  const char* P8 = static_cast<const char*>(params);
+  const int N = (int)sc.N;
+
+  // schedule tables for the time reversal (built on the device from the
+  // lengths passed by value); a zero initial cell state
+  {
+    am::SchedTables st;
+    memset(&st, 0, sizeof st);
+    st.T = T; st.B = B;
+    for (int b = 0; b < B; ++b) st.len[b] = (uint16_t)sc.lens[b];
+    st.offs = at<int64_t>(ws, w.offs);
+    st.lens = at<int32_t>(ws, w.lens);
+    AM_TRY(hip_check(am::schedule_tables(st, s), "schedule tables"));
+  }
+  AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.c0), B * H, s), "c0 clear"));
+  AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_BYTES / 4, s), "sync clear"));
+  auto gather = [&](const void* src, int64_t src_ld, void* dst, int64_t dst_ld, int64_t col,
+                    int width, bool reverse) {
+    am::GatherRows g;
+    g.src = src; g.src_ld = src_ld; g.dst = dst; g.dst_ld = dst_ld; g.dst_col = col;
+    g.width = width; g.N = sc.N; g.T = T;
+    g.offs = at<int64_t>(ws, w.offs); g.lens = at<int32_t>(ws, w.lens);
+    g.reverse = reverse ? 1 : 0;
+    Timed tm(AM_K_MISC, s, 0.0, 2.0 * sc.N * width * e);
+    return hip_check(am::gather_rows(g, bf, s), "gather rows");
+  };
+
+  for (int l = 0; l < L; ++l) {
+    const int64_t D = l == 0 ? m->input_dim : 2 * H;
+    const void* X = l == 0 ? x : at<void>(ws, (l - 1) % 2 ? w.cat1 : w.cat0);
+    void* out = at<void>(ws, l % 2 ? w.cat1 : w.cat0);
+    for (int d = 0; d < 2; ++d) {
+      const int k = 2 * l + d;
+      const void* in = X;
+      if (d == 1) {  // the backward direction reads the sequences reversed
+        AM_TRY(gather(X, D, at<void>(ws, w.rev), D, 0, (int)D, true));
+        in = at<void>(ws, w.rev);
+      }
+      AM_TRY(run_gemm(AM_K_GEMM_FWD,
+                      mk_gemm(in, D, true, P8 + po.wx[k] * e, D, true, at<void>(ws, w.p), G, false,
+                              P8 + po.b[k] * e, N, (int)G, (int)D, bf), s));
+      FwdLayer f;
+      f.P = at<void>(ws, w.p);
+      f.Wh = P8 + po.wh[k] * e;
+      f.h0 = nullptr;
+      f.c0 = at<float>(ws, w.c0);
+      f.H = at<void>(ws, w.hdir);
+      f.Hs = at<void>(ws, w.hs);
+      f.C = at<float>(ws, w.c);
+      f.G = at<void>(ws, w.g);
+      f.sync = at<void>(ws, w.sync);
+      AM_TRY(forward_recurrence(f, sc, bf, H, s));
+      AM_TRY(gather(at<void>(ws, w.hdir), H, out, 2 * H, d * H, (int)H, d == 1));
+    }
+  }
+  return run_gemm(AM_K_GEMM_FWD,
+                  mk_gemm(at<void>(ws, (L - 1) % 2 ? w.cat1 : w.cat0), 2 * H, true, P8 + po.wo * e,
+                          2 * H, true, logits, m->classes, true, P8 + po.bo * e, N, m->classes,
+                          (int)(2 * H), bf), s);
+}
+
+am_status kbest_logits(int64_t N, int32_t C, int32_t K, const float* logits, int32_t* idx,
+                       float* val, void* stream) {
+  if (N < 0 || C < 1 || K < 0 || K > C) return fail(AM_EINVAL, "need N >= 0, C >= 1, 0 <= K <= C");
+  if (K > 64) return fail(AM_EUNSUPPORTED, "K > 64");
+  if (C > 8192) return fail(AM_EUNSUPPORTED, "C > 8192");
+  if (N > 0 && K > 0 && (!logits || !idx || !val)) return fail(AM_EINVAL, "NULL pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Timed tm(AM_K_MISC, s, 0.0, (double)N * (4.0 * C + 8.0 * K));
+  return hip_check(am::topk_rows(N, C, K, logits, idx, val, s), "kbest_logits");
+}
+
+am_status kbest_posteriors(int64_t N, int32_t K, const float* val, float* prob, void* stream) {
+  if (N < 0 || K < 0) return fail(AM_EINVAL, "need N >= 0 and K >= 0");
+  if (N > 0 && K > 0 && (!val || !prob)) return fail(AM_EINVAL, "NULL pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Timed tm(AM_K_MISC, s, 0.0, (double)N * 8.0 * K);
+  return hip_check(am::kbest_posteriors(N, K, val, prob, s), "kbest_posteriors");
+}
+
 am_status sparse_soft_ce(int64_t N, int32_t C, int32_t K, const float* logits, const int32_t* idx,
                          const float* prob, const uint8_t* mask, int32_t reduction, float* loss,
                          void* dlogits, int32_t dlogits_dtype, void* ws, int64_t ws_bytes,
@@ -579,66 +831,17 @@ am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
     AM_TRY(run_gemm(AM_K_GEMM_FWD,
                     mk_gemm(X, D, true, P8 + po.wx[l] * e, D, true, P, G, false, P8 + po.b[l] * e,
                             (int)sc.N, (int)G, (int)D, bf), s));
-    const char* Hl = at<char>(ws, w.h[l]);
-    const float* Cl = at<float>(ws, w.c[l]);
-    if (sc.N > 0 && persistent_enabled()) {
-      am::PersistFwd pa;
-      pa.P = at<void>(ws, w.p_da);
-      pa.Wh = P8 + po.wh[l] * e;
-      pa.h0 = h0 ? at<char>(ws, w.h0) + (int64_t)l * B * H * e : nullptr;
-      pa.c0 = at<float>(ws, w.c0) + (int64_t)l * B * H;
-      pa.H = at<void>(ws, w.h[l]);
-      pa.Hs = at<void>(ws, w.hs[l]);
-      pa.C = at<float>(ws, w.c[l]);
-      pa.G = at<void>(ws, w.g[l]);
-      pa.counters = at<unsigned>(ws, w.sync);
-      pa.err = at<int>(ws, w.sync) + SYNC_STICKY_WORD;
-      pa.hidden = (int)H;
-      const am::PersistSchedule ps = persist_schedule(sc);
-      const double flops = 2.0 * sc.N * G * H;
-      const double bytes = (double)sc.N * (G * e * 2 + H * (2 * e + 4)) + (double)G * H * e;
-      bool used = false;
-      if (bf && xcd_enabled() && am::lstm_xcd_instantiated(true, (int)H, B)) {
-        AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
-        Timed tm(AM_K_LSTM_FWD, s, flops, bytes);
-        AM_TRY(hip_check(am::lstm_fwd_xcd_launch(pa, ps, xcd_sync(at<void>(ws, w.sync)), s, &used),
-                         "lstm forward layer (xcd)"));
-        if (!used) tm.cancel();
-      }
-      if (!used && device_persistent_enabled() && am::lstm_persistent_fits(true, (int)H, B, bf, T)) {
-        AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
-        Timed tm(AM_K_LSTM_FWD, s, flops, bytes);
-        AM_TRY(hip_check(am::lstm_fwd_persistent(pa, ps, bf, s, &used), "lstm forward layer"));
-        if (!used) tm.cancel();
-      }
-      if (used) continue;
-    }
-    for (int t = 0; t < T; ++t) {
-      const int64_t nb = sc.counts[t];
-      if (nb == 0) break;
-      const int64_t o = sc.offs[t];
-      am::LstmFwdStep a;
-      a.P = at<char>(ws, w.p_da) + o * G * e;
-      a.Wh = P8 + po.wh[l] * e;
-      if (t == 0) {
-        a.hprev = h0 ? at<char>(ws, w.h0) + (int64_t)l * B * H * e : nullptr;
-        a.cprev = at<float>(ws, w.c0) + (int64_t)l * B * H;
-      } else {
-        a.hprev = Hl + sc.offs[t - 1] * H * e;
-        a.cprev = Cl + sc.offs[t - 1] * H;
-      }
-      a.H = at<char>(ws, w.h[l]) + o * H * e;
-      a.Hs = at<char>(ws, w.hs[l]) + o * H * e;
-      a.C = at<float>(ws, w.c[l]) + o * H;
-      a.G = at<char>(ws, w.g[l]) + o * G * e;
-      a.nb = (int)nb;
-      a.hidden = (int)H;
-      a.bf16 = bf;
-      const double bytes = (double)(nb * H + G * H + nb * G) * e + nb * H * 4.0 +
-                           (double)nb * (H * (2 * e + 4) + G * e);
-      Timed tm(AM_K_LSTM_FWD, s, 2.0 * nb * G * H, bytes);
-      AM_TRY(hip_check(am::lstm_fwd_step(a, s), "lstm forward step"));
-    }
+    FwdLayer f;
+    f.P = at<void>(ws, w.p_da);
+    f.Wh = P8 + po.wh[l] * e;
+    f.h0 = h0 ? at<char>(ws, w.h0) + (int64_t)l * B * H * e : nullptr;
+    f.c0 = at<float>(ws, w.c0) + (int64_t)l * B * H;
+    f.H = at<void>(ws, w.h[l]);
+    f.Hs = at<void>(ws, w.hs[l]);
+    f.C = at<float>(ws, w.c[l]);
+    f.G = at<void>(ws, w.g[l]);
+    f.sync = at<void>(ws, w.sync);
+    AM_TRY(forward_recurrence(f, sc, bf, H, s));
   }
   AM_TRY(run_gemm(AM_K_GEMM_FWD,
                   mk_gemm(at<void>(ws, w.h[L - 1]), H, true, P8 + po.wo * e, H, true, logits,

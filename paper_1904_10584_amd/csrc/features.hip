@@ -28,11 +28,15 @@ template <typename T> __device__ __forceinline__ T from_f64(double v);
 template <> __device__ __forceinline__ float from_f64<float>(double v) { return (float)v; }
 template <> __device__ __forceinline__ bf16_t from_f64<bf16_t>(double v) { return f32_to_bf16((float)v); }
 
-// Packed row offset of frame t: off_t = sum over sequences of min(len_b, t).
-__device__ __forceinline__ int64_t packed_offset(const uint16_t* len, int B, int t) {
-  int64_t o = 0;
-  for (int b = 0; b < B; ++b) o += len[b] < t ? len[b] : t;
-  return o;
+// Sum of one value per thread over a 256-thread workgroup (all threads get
+// it).  `red` is 4 LDS slots; the call contains two barriers.
+__device__ __forceinline__ int64_t block_sum(int64_t v, int64_t* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  __syncthreads();  // earlier readers of red are done
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
 }
 
 template <typename OutT>
@@ -41,20 +45,17 @@ __global__ __launch_bounds__(256) void lfr_features_kernel(LfrArgs a) {
   const int b = blockIdx.x;
   const int D = a.stack * a.raw_dim;
   __shared__ uint16_t T_len[1024];
-  __shared__ int64_t s_raw0;
+  __shared__ int64_t red[4];
+  int64_t r0 = 0;  // raw frames of the utterances before this one
   for (int i = threadIdx.x; i < a.B; i += blockDim.x) {
     const int U = a.U[i];
     const int T = (U - a.offset - a.stack) / a.skip + 1;
     T_len[i] = (uint16_t)(U - a.offset - a.stack >= 0 ? T : 0);
+    if (i < b) r0 += U;
   }
-  if (threadIdx.x == 0) {
-    int64_t r0 = 0;
-    for (int i = 0; i < b; ++i) r0 += a.U[i];
-    s_raw0 = r0;
-  }
-  __syncthreads();
+  r0 = block_sum(r0, red);  // its barriers also publish T_len
   const int Tb = T_len[b];
-  const float* __restrict__ raw = a.raw + s_raw0 * a.raw_dim;
+  const float* __restrict__ raw = a.raw + r0 * a.raw_dim;
   OutT* __restrict__ x = static_cast<OutT*>(a.x);
   for (int j = threadIdx.x; j < D; j += blockDim.x) {
     const int k = j / a.raw_dim, d = j % a.raw_dim;
@@ -88,17 +89,20 @@ __global__ __launch_bounds__(256) void lfr_features_kernel(LfrArgs a) {
 
 __global__ __launch_bounds__(256) void delay_targets_kernel(DelayArgs a) {
   const int t = blockIdx.x;
-  __shared__ int64_t s_off, s_src;
-  __shared__ int s_nb;
-  if (threadIdx.x == 0) {
-    s_off = packed_offset(a.len, a.B, t);
-    s_src = t >= a.delay ? packed_offset(a.len, a.B, t - a.delay) : 0;
-    int nb = 0;
-    for (int b = 0; b < a.B; ++b) nb += a.len[b] > t;
-    s_nb = nb;
+  __shared__ int64_t red[4];
+  // packed offsets of frames t and t - delay (off_t = sum of min(len_b, t))
+  // and the sequences active at t
+  const int ts = t >= a.delay ? t - a.delay : 0;
+  int64_t o = 0, os = 0, c = 0;
+  for (int b = threadIdx.x; b < a.B; b += blockDim.x) {
+    const int len = a.len[b];
+    o += len < t ? len : t;
+    os += len < ts ? len : ts;
+    c += len > t;
   }
-  __syncthreads();
-  const int nb = s_nb;
+  const int64_t s_off = block_sum(o, red);
+  const int64_t s_src = block_sum(os, red);
+  const int nb = (int)block_sum(c, red);
   const bool has = t >= a.delay;
   for (int e = threadIdx.x; e < nb * a.K; e += blockDim.x) {
     const int b = e / a.K, q = e % a.K;

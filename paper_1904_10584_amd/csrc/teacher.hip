@@ -1,0 +1,179 @@
+// Teacher target generation (§V-A, §V-C): the pieces the bidirectional
+// teacher adds to the student's kernels, and the k-best logits.
+//
+// gather_rows: copies the packed rows of a batch, optionally reversing each
+// sequence in time (row (t, b) takes row (len_b - 1 - t, b)), into a column
+// range of another matrix.  The teacher's backward direction runs the
+// student's forward recurrence on the time-reversed input projections and
+// writes its hidden states back in time order next to the forward
+// direction's.  One thread per 16-byte chunk; a row's frame index comes from
+// a binary search in the packed row offsets.
+//
+// topk_rows: the k largest logits of each row in descending order (equal
+// values by ascending index, NaN after every number), one wave per row with
+// the row held in registers; k rounds of a wave-wide arg-max over the
+// entries not yet taken.
+//
+// kbest_posterior_rows: the posterior rebuilt from k stored logits with the
+// missing ones at -infinity, i.e. the softmax over the k values (fp32).
+#include <cmath>
+
+#include "am_device.h"
+#include "am_internal.h"
+
+namespace am {
+namespace {
+
+// Device copies of a batch's schedule: offs[t] = sum_b min(len_b, t) for
+// t = 0..T, and the lengths.
+__global__ __launch_bounds__(256) void schedule_tables_kernel(SchedTables a) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t <= a.T) {
+    int64_t o = 0;
+    for (int b = 0; b < a.B; ++b) o += a.len[b] < t ? a.len[b] : t;
+    a.offs[t] = o;
+  }
+  if (t < a.B) a.lens[t] = a.len[t];
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void gather_rows_kernel(GatherRows a) {
+  constexpr int EPC = 16 / sizeof(T);
+  const int cpr = a.width / EPC;
+  const int64_t total = a.N * cpr;
+  const T* __restrict__ src = static_cast<const T*>(a.src);
+  T* __restrict__ dst = static_cast<T*>(a.dst);
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int64_t r = e / cpr;
+    const int c = (int)(e % cpr);
+    int64_t sr = r;
+    if (a.reverse) {
+      // frame t of row r: the last t with offs[t] <= r
+      int lo = 0, hi = a.T - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (a.offs[mid] <= r) lo = mid; else hi = mid - 1;
+      }
+      const int b = (int)(r - a.offs[lo]);
+      sr = a.offs[a.lens[b] - 1 - lo] + b;
+    }
+    const uint4 v = *reinterpret_cast<const uint4*>(src + sr * a.src_ld + c * EPC);
+    *reinterpret_cast<uint4*>(dst + r * a.dst_ld + a.dst_col + c * EPC) = v;
+  }
+}
+
+// (va, ia) ranks before (vb, ib): numbers before NaN, larger first, then
+// the lower index.
+__device__ __forceinline__ bool ranks_before(float va, int ia, float vb, int ib) {
+  const bool na = va != va, nb = vb != vb;
+  if (na != nb) return nb;
+  if (!na && va != vb) return va > vb;
+  return ia < ib;
+}
+
+template <int CPL>
+__global__ __launch_bounds__(256) void topk_rows_kernel(int64_t N, int C, int K,
+                                                        const float* __restrict__ z,
+                                                        int32_t* __restrict__ idx,
+                                                        float* __restrict__ val) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= N) return;
+  const float* zr = z + row * C;
+  float v[CPL];
+  uint64_t taken[(CPL + 63) / 64];
+#pragma unroll
+  for (int q = 0; q < (CPL + 63) / 64; ++q) taken[q] = 0;
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
+    const int c = lane + 64 * q;
+    v[q] = c < C ? zr[c] : 0.f;
+    if (c >= C) taken[q >> 6] |= 1ull << (q & 63);
+  }
+  for (int j = 0; j < K; ++j) {
+    float bv = 0.f;
+    int bi = 0x7FFFFFFF;  // none
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      if (taken[q >> 6] & (1ull << (q & 63))) continue;
+      const int c = lane + 64 * q;
+      if (bi == 0x7FFFFFFF || ranks_before(v[q], c, bv, bi)) { bv = v[q]; bi = c; }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (oi != 0x7FFFFFFF && (bi == 0x7FFFFFFF || ranks_before(ov, oi, bv, bi))) { bv = ov; bi = oi; }
+    }
+    if (bi == 0x7FFFFFFF) {  // fewer than K entries: empty slots
+      if (lane == 0) { idx[row * K + j] = -1; val[row * K + j] = -INFINITY; }
+      continue;
+    }
+    if ((bi & 63) == lane) {
+      const int q = bi >> 6;
+#pragma unroll
+      for (int qq = 0; qq < CPL; ++qq)
+        if (qq == q) taken[qq >> 6] |= 1ull << (qq & 63);
+    }
+    if (lane == 0) { idx[row * K + j] = bi; val[row * K + j] = bv; }
+  }
+}
+
+__global__ __launch_bounds__(256) void kbest_posterior_rows(int64_t N, int K,
+                                                            const float* __restrict__ val,
+                                                            float* __restrict__ prob) {
+  const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (row >= N) return;
+  const float* v = val + row * K;
+  float m = -INFINITY;
+  for (int j = 0; j < K; ++j) m = fmaxf(m, v[j]);
+  float s = 0.f;
+  for (int j = 0; j < K; ++j) s += expf(v[j] - m);
+  for (int j = 0; j < K; ++j) prob[row * K + j] = expf(v[j] - m) / s;
+}
+
+}  // namespace
+
+hipError_t schedule_tables(const SchedTables& a, hipStream_t s) {
+  const int n = (a.T + 1 > a.B ? a.T + 1 : a.B);
+  hipLaunchKernelGGL(schedule_tables_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t gather_rows(const GatherRows& a, bool bf16, hipStream_t s) {
+  const int epc = bf16 ? 8 : 4;
+  const int64_t total = a.N * (a.width / epc);
+  if (total == 0) return hipSuccess;
+  const int64_t want = (total + 255) / 256;
+  const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
+  if (bf16)
+    hipLaunchKernelGGL(gather_rows_kernel<bf16_t>, dim3(grid), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(gather_rows_kernel<float>, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+#define AM_TOPK_CASE(CPL_)                                                                    \
+  if (cpl <= CPL_) {                                                                          \
+    hipLaunchKernelGGL(topk_rows_kernel<CPL_>, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, s, \
+                       N, C, K, z, idx, val);                                                 \
+    return hipGetLastError();                                                                 \
+  }
+
+hipError_t topk_rows(int64_t N, int C, int K, const float* z, int32_t* idx, float* val,
+                     hipStream_t s) {
+  if (N == 0 || K == 0) return hipSuccess;
+  const int cpl = (C + 63) / 64;
+  AM_TOPK_CASE(16) AM_TOPK_CASE(32) AM_TOPK_CASE(48) AM_TOPK_CASE(64) AM_TOPK_CASE(96)
+  AM_TOPK_CASE(128)
+  return hipErrorInvalidValue;
+}
+
+hipError_t kbest_posteriors(int64_t N, int K, const float* val, float* prob, hipStream_t s) {
+  if (N == 0 || K == 0) return hipSuccess;
+  hipLaunchKernelGGL(kbest_posterior_rows, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, s, N,
+                     K, val, prob);
+  return hipGetLastError();
+}
+
+}  // namespace am

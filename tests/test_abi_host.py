@@ -167,3 +167,31 @@ def test_bmuf_and_multi_decode_argument_checks(L):
     assert st == -1
     st, _ = _status(L, "grad_threshold_decode_multi", 4, fake, n, fake, f(1e-3), 1 << 31, fake, 0, fake, ws, None)
     assert st == -1
+
+
+@pytest.mark.parametrize("dims", [(2, 64, 64, 500), (5, 192, 768, 3000), (1, 8, 16, 8)])
+def test_teacher_layout_matches_oracle(dims):
+    L_, D, H, C = dims
+    m = am.Model(L_, D, H, C, am.BF16 if D % 8 == 0 and C % 8 == 0 else am.F32)
+    td = oracle.TeacherDims(L_, D, H, C)
+    assert am.teacher_param_count(m) == oracle.teacher_param_count(td)
+    assert am.teacher_param_offsets(m) == oracle.teacher_param_offsets(td)
+
+
+def test_teacher_argument_checks(L):
+    fake = ctypes.c_void_p(0x100000)
+    m = _m(2, 64, 64, 520, am.BF16)
+    ws = L.am_teacher_workspace_bytes(ctypes.byref(m), 10, 4, 40)
+    assert ws > 0 and ws % 256 == 0
+    st, _ = _status(L, "blstm_teacher_forward", ctypes.byref(m), fake, fake, None, 10, 4, fake, fake, ws - 1, None)
+    assert st == -5
+    st, _ = _status(L, "blstm_teacher_forward", ctypes.byref(m), fake, fake, None, 10, 2000, fake, fake, ws, None)
+    assert st == -3
+    st, _ = _status(L, "kbest_logits", 10, 100, 101, fake, fake, fake, None)
+    assert st == -1   # K > C
+    st, _ = _status(L, "kbest_logits", 10, 100, 65, fake, fake, fake, None)
+    assert st == -3   # K > 64
+    st, _ = _status(L, "kbest_logits", 10, 9000, 20, fake, fake, fake, None)
+    assert st == -3   # C > 8192
+    st, _ = _status(L, "kbest_posteriors", -1, 20, fake, fake, None)
+    assert st == -1
