@@ -37,7 +37,8 @@ def parse():
     ap.add_argument("--workload", default="paper-5x768")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-worker-kernels", action="store_true",
-                    help="skip timing the side kernels (BMUF step, 8-stream aggregate, input features, target delay)")
+                    help="skip timing the side kernels (BMUF step, 8-stream aggregate, input features, "
+                         "target delay, teacher target generation)")
     ap.add_argument("--cpu-chunks", type=int, default=0,
                     help="chunks the CPU oracle runs forward/backward on (0 = the whole batch)")
     return ap.parse_args()
@@ -205,6 +206,49 @@ def input_kernels(am, synth, w, N, reps):
     return out
 
 
+def teacher_kernels(am, synth, w, reps):
+    """Target generation for one batch of the workload (outside the timed
+    step): the bidirectional LSTM teacher of the same depth and width as the
+    student (each direction of each layer `hidden` cells), its logits' k best
+    entries and the posteriors rebuilt from them."""
+    import torch
+    T, B, K, C = w["T"], w["B"], w["K"], w["classes"]
+    m = am.Model(w["layers"], w["input_dim"], w["hidden"], C, am.BF16)
+    n = am.teacher_param_count(m)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(8)
+    bound = 1.0 / w["hidden"] ** 0.5
+    params = ((torch.rand(n, generator=gen, device="cuda") * 2 - 1) * bound).to(torch.bfloat16)
+    x = torch.randn((T * B, w["input_dim"]), generator=gen, device="cuda").to(torch.bfloat16)
+    logits = torch.empty((T * B, C), dtype=torch.float32, device="cuda")
+    ws = torch.empty(am.teacher_workspace_bytes(m, T, B, T * B), dtype=torch.uint8, device="cuda")
+    idx = torch.empty((T * B, K), dtype=torch.int32, device="cuda")
+    val = torch.empty((T * B, K), dtype=torch.float32, device="cuda")
+    prob = torch.empty_like(val)
+    am.blstm_teacher_forward(m, params, x, T, B, logits, ws)  # warm-up
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        am.blstm_teacher_forward(m, params, x, T, B, logits, ws)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    am.workspace_check(ws)
+    out = {"teacher_forward": {"ms_per_batch": round(dt * 1e3, 3),
+                               "frames_per_s": round(T * B / dt, 1),
+                               "params": n, "frames": T * B}}
+    am.profile_begin([am.K_MISC])
+    for _ in range(reps):
+        am.kbest_logits(logits, idx, val)
+    am.profile_end()
+    out["kbest_logits"] = dict(_hbm_entry(am.profile_get(am.K_MISC), reps), k=K)
+    am.profile_begin([am.K_MISC])
+    for _ in range(reps):
+        am.kbest_posteriors(val, prob)
+    am.profile_end()
+    out["kbest_posteriors"] = dict(_hbm_entry(am.profile_get(am.K_MISC), reps), k=K)
+    return out
+
+
 def cpu_baseline(wl, synth, chunks):
     """The oracle, as it stands, on a bounded sample: forward, CE and BPTT on
     `chunks` chunks of the batch, plus encode, decode and SGD of the whole
@@ -334,6 +378,8 @@ def main():
         out["worker_kernels"] = worker_kernels(am, st.n, reps=10)
         if lengths is None:
             out["input_kernels"] = input_kernels(am, synth, w, N, reps=10)
+            if bf16:
+                out["teacher_kernels"] = teacher_kernels(am, synth, w, reps=5)
     if not args.no_cpu_baseline and args.workload in ("paper-5x768", "tiny-2x64", "wide-5x1536"):
         out["cpu_baseline"] = cpu_baseline(args.workload, synth, args.cpu_chunks)
     print(json.dumps(out), flush=True)
