@@ -11,8 +11,8 @@
 //
 // topk_rows: the k largest logits of each row in descending order (equal
 // values by ascending index, NaN after every number), one wave per row with
-// the row held in registers; k rounds of a wave-wide arg-max over the
-// entries not yet taken.
+// the row held in registers as order-preserving integer keys; k rounds of a
+// wave-wide arg-max over the entries not yet taken.
 //
 // kbest_posterior_rows: the posterior rebuilt from k stored logits with the
 // missing ones at -infinity, i.e. the softmax over the k values (fp32).
@@ -62,13 +62,14 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(GatherRows a) {
   }
 }
 
-// (va, ia) ranks before (vb, ib): numbers before NaN, larger first, then
-// the lower index.
-__device__ __forceinline__ bool ranks_before(float va, int ia, float vb, int ib) {
-  const bool na = va != va, nb = vb != vb;
-  if (na != nb) return nb;
-  if (!na && va != vb) return va > vb;
-  return ia < ib;
+// Order-preserving key of a logit: larger values get larger keys, -0 and +0
+// the same key, NaN key 1 (below every number), and 0 marks an entry already
+// taken.  A wave-wide candidate is (key << 32) | ~index, so equal keys rank
+// the lower index first.
+__device__ __forceinline__ uint32_t logit_key(float f) {
+  if (f != f) return 1u;
+  uint32_t u = __float_as_uint(f == 0.f ? 0.f : f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
 template <int CPL>
@@ -80,42 +81,39 @@ __global__ __launch_bounds__(256) void topk_rows_kernel(int64_t N, int C, int K,
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= N) return;
   const float* zr = z + row * C;
-  float v[CPL];
-  uint64_t taken[(CPL + 63) / 64];
-#pragma unroll
-  for (int q = 0; q < (CPL + 63) / 64; ++q) taken[q] = 0;
+  uint32_t key[CPL];
 #pragma unroll
   for (int q = 0; q < CPL; ++q) {
     const int c = lane + 64 * q;
-    v[q] = c < C ? zr[c] : 0.f;
-    if (c >= C) taken[q >> 6] |= 1ull << (q & 63);
+    key[q] = c < C ? logit_key(zr[c]) : 0u;
   }
   for (int j = 0; j < K; ++j) {
-    float bv = 0.f;
-    int bi = 0x7FFFFFFF;  // none
+    // this lane's best: the largest key, the first (lowest index) on ties
+    uint32_t bk = 0u;
+    int bq = 0;
 #pragma unroll
     for (int q = 0; q < CPL; ++q) {
-      if (taken[q >> 6] & (1ull << (q & 63))) continue;
-      const int c = lane + 64 * q;
-      if (bi == 0x7FFFFFFF || ranks_before(v[q], c, bv, bi)) { bv = v[q]; bi = c; }
+      const bool better = key[q] > bk;
+      bk = better ? key[q] : bk;
+      bq = better ? q : bq;
     }
+    uint64_t cand = bk ? ((uint64_t)bk << 32) | (uint32_t)~(uint32_t)(lane + 64 * bq) : 0ull;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      if (oi != 0x7FFFFFFF && (bi == 0x7FFFFFFF || ranks_before(ov, oi, bv, bi))) { bv = ov; bi = oi; }
+      const uint64_t other = __shfl_xor(cand, o, 64);
+      cand = other > cand ? other : cand;
     }
-    if (bi == 0x7FFFFFFF) {  // fewer than K entries: empty slots
+    if (cand == 0ull) {  // fewer than K entries
       if (lane == 0) { idx[row * K + j] = -1; val[row * K + j] = -INFINITY; }
       continue;
     }
-    if ((bi & 63) == lane) {
-      const int q = bi >> 6;
+    const int c = (int)~(uint32_t)cand;
+    if ((c & 63) == lane) {
 #pragma unroll
-      for (int qq = 0; qq < CPL; ++qq)
-        if (qq == q) taken[qq >> 6] |= 1ull << (qq & 63);
+      for (int q = 0; q < CPL; ++q)
+        if (q == (c >> 6)) key[q] = 0u;
     }
-    if (lane == 0) { idx[row * K + j] = bi; val[row * K + j] = bv; }
+    if (lane == 0) { idx[row * K + j] = c; val[row * K + j] = zr[c]; }
   }
 }
 
