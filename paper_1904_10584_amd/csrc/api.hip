@@ -197,13 +197,14 @@ constexpr int64_t SYNC_STICKY_WORD = SYNC_BYTES / 4 - 1;
 am::XcdSync xcd_sync(void* base) {
   unsigned* u = static_cast<unsigned*>(base);
   am::XcdSync y;
-  y.flags = u;             // counter of block k at u[32 k]
-  y.start = u + 256;
+  y.flags = u;             // counter of block k < 16 at u[32 k]
+  y.start = u + 512;
   y.err = reinterpret_cast<int*>(u + SYNC_STICKY_WORD);
-  y.xcc = reinterpret_cast<int*>(u + 260);  // up to 1024 workgroups
+  y.xcc = reinterpret_cast<int*>(u + 516);  // up to 1024 workgroups
   y.units = 0;
   return y;
 }
+static_assert(516 + 1024 <= SYNC_CLEAR_WORDS, "sync region: counters, start word and XCC ids are cleared");
 
 am::PersistSchedule persist_schedule(const Schedule& sc) {
   am::PersistSchedule ps;

@@ -4,11 +4,12 @@
 // workgroups that share a block of sequences at every step.  MI355X has 8
 // XCDs, each with its own L2; an exchange through device memory pays a
 // write-back of the producer's L2, an invalidation of the consumer's, and
-// memory latency on every step.  Here the sequences are split into 8 blocks,
-// one per XCD, and the workgroups of a block all run on that XCD, so the
-// exchange and the step barrier stay inside one L2:
-//   * workgroup i serves block i % 8 and unit slice i / 8 (workgroups are
-//     dispatched to XCDs round-robin); at start every workgroup records its
+// memory latency on every step.  Here the sequences are split into blocks,
+// one or two per XCD, and the workgroups of a block all run on that XCD, so
+// the exchange and the step barrier stay inside one L2:
+//   * with m workgroups per block, workgroup i serves block i % 8 + 8 (i / 8m)
+//     and unit slice (i / 8) % m (workgroups are dispatched to XCDs
+//     round-robin); at start every workgroup records its
 //     XCC id and, unless every block really is on one XCD, the kernel falls
 //     back to device-scope release/acquire for its whole run;
 //   * the step barrier is one counter per block, bumped with an atomic add
@@ -23,6 +24,8 @@
 // through LDS then gives each lane all four gate pre-activations of one
 // (sequence, unit).  The backward product keeps the U columns of W_h in
 // registers too.
+#include <cstdlib>
+
 #include "am_device.h"
 #include "am_internal.h"
 
@@ -70,11 +73,11 @@ __device__ bool check_local(const XcdSync& y, int* bad_sh) {
 // or the memory side), so counter updates are seen by every poller; the
 // release fence (a write-back of this XCD's L2) is needed only when a block
 // spans XCDs.
-__device__ __forceinline__ void xsignal(const XcdSync& y, bool local) {
+__device__ __forceinline__ void xsignal(const XcdSync& y, bool local, int blk) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
-    unsigned* cnt = y.flags + (blockIdx.x % NX) * 32;
+    unsigned* cnt = y.flags + blk * 32;
     if (!local) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -84,9 +87,9 @@ __device__ __forceinline__ void xsignal(const XcdSync& y, bool local) {
 // lane polls with device-scope loads, which bypass the CU's L1; the other
 // workgroups' exchanged rows are then read from the shared L2 (local) or
 // after an acquire that invalidates this CU's caches (block spans XCDs).
-__device__ __forceinline__ void xwait(const XcdSync& y, bool local, unsigned target) {
+__device__ __forceinline__ void xwait(const XcdSync& y, bool local, int blk, unsigned target) {
   if (threadIdx.x == 0) {
-    const unsigned* cnt = y.flags + (blockIdx.x % NX) * 32;
+    const unsigned* cnt = y.flags + blk * 32;
     unsigned spins = 0;
     while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
       if (++spins > SPIN_LIMIT) {
@@ -98,6 +101,13 @@ __device__ __forceinline__ void xwait(const XcdSync& y, bool local, unsigned tar
     if (!local) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
   __syncthreads();
+}
+
+// Block of sequences served by this workgroup: workgroup i runs on XCD
+// i % 8 and serves block i % 8 + 8 (i / 8 / members), so with two blocks per
+// XCD both of them sit on the XCD of their workgroups.
+__device__ __forceinline__ int xcd_block(int members) {
+  return (int)(blockIdx.x % NX) + NX * (int)(blockIdx.x / NX / members);
 }
 
 __device__ __forceinline__ int active_down(const PersistSchedule& ps, int nb, int t) {
@@ -142,9 +152,9 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
   const int g = wave & 3, kh = wave >> 2;
   const int H = KS * 32, G4 = 4 * H, U = y.units;
   const int ntiles = MT * (U / 4);
-  const int blk = blockIdx.x % NX, us = blockIdx.x / NX;
-  const int b0 = blk * RB, j0 = us * U;
   const int members = H / U;
+  const int blk = xcd_block(members), us = (blockIdx.x / NX) % members;
+  const int b0 = blk * RB, j0 = us * U;
   const int mw = g % MT;
   const int ts_lo = kh == 0 ? 0 : FIN, ts_hi = kh == 0 ? FIN : TPW;
   const bf16_t* __restrict__ P = static_cast<const bf16_t*>(a.P);
@@ -206,7 +216,7 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
     for (int ts = 0; ts < TPW; ++ts) acc[ts] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     const bf16_t* hsrc = h0;
     if (t > 0) {
-      xwait(y, local, (unsigned)(members * t));
+      xwait(y, local, blk, (unsigned)(members * t));
       hsrc = Hb + (int64_t)off_prev * H;
     }
     if (hsrc) {
@@ -288,7 +298,7 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
         h_reg[o] = h;
       }
     }
-    xsignal(y, local);  // h stores complete; its barrier also orders the LDS reuse
+    xsignal(y, local, blk);  // h stores complete; its barrier also orders the LDS reuse
     // stores only the backward pass reads
 #pragma unroll
     for (int o = 0; o < FIN; ++o) {
@@ -333,9 +343,9 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int H = a.hidden, G4 = 4 * H, U = y.units;
-  const int blk = blockIdx.x % NX, us = blockIdx.x / NX;
-  const int b0 = blk * RB, j0 = us * U;
   const int members = H / U;
+  const int blk = xcd_block(members), us = (blockIdx.x / NX) % members;
+  const int b0 = blk * RB, j0 = us * U;
   const bf16_t* __restrict__ WhT = static_cast<const bf16_t*>(a.WhT);
   const bf16_t* __restrict__ dHa = static_cast<const bf16_t*>(a.dHa);
   const bf16_t* __restrict__ Gb = static_cast<const bf16_t*>(a.G);
@@ -401,7 +411,7 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
 #pragma unroll
       for (int n = 0; n < NTU; ++n) acc[m][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (b0 < nb_next) {
-      xwait(y, local, (unsigned)members * done);
+      xwait(y, local, blk, (unsigned)members * done);
       const bf16_t* dAn = dA + (int64_t)off_next * G4 + wave * KW * 32;
       // chunk c of this wave's k-slice into buffer bi: RB rows x CH k-steps;
       // instruction i covers rows i*(64/CPR) .., 16-byte pieces swizzled by row
@@ -472,17 +482,18 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
       arow[2 * H + j] = f32_to_bf16(d_g * (1.f - vg * vg));
       arow[3 * H + j] = f32_to_bf16(d_o * vo * (1.f - vo));
     }
-    xsignal(y, local);  // its barrier also orders the LDS reuse
+    xsignal(y, local, blk);  // its barrier also orders the LDS reuse
     ++done;
   }
 }
 
 // ------------------------------------------------------------------ launch --
 
-int xcd_units(int H) {
-  // workgroups per XCD = H / U <= 32, U a multiple of 4
+// Units per workgroup: the least multiple of 4 dividing H with at most
+// `members` workgroups per block.
+int xcd_units(int H, int members) {
   for (int U = 4; U <= H; U += 4)
-    if (H % U == 0 && H / U <= 32) return U;
+    if (H % U == 0 && H / U <= members) return U;
   return 0;
 }
 
@@ -508,12 +519,16 @@ hipError_t coop(K kernel, int blocks, int threads, size_t lds, void** args, hipS
   return resident_launch(fn, dim3(blocks), dim3(threads), args, lds, s);
 }
 
-// Shapes covered: bf16 (the resident slices are sized for it), RB = 16 or
-// 32 sequences per block (B <= 256), hidden sizes with H % 64 == 0, the
-// forward weight slice within the register budget and the backward one
-// within the LDS budget.
+// Shapes covered: bf16 (the resident slices are sized for it), B <= 256,
+// hidden sizes with H % 64 == 0 and the resident weight slices within the
+// register budget.  Blocks hold RB = 16 MT sequences; BPX blocks share an
+// XCD, each served by 32 / BPX workgroups.  B > 128 takes blocks of 16, two
+// per XCD (AM_XCD_BLOCKS=1 in the environment selects blocks of 32, one per
+// XCD): per step each workgroup then reads half as many exchanged bytes
+// (16 rows instead of 32) for twice as many units, and the backward's unit
+// tiles are full (48 units = 3 x 16 instead of 24 = 16 + 8).
 struct XShape {
-  int MT, KS, U, NT, TPW, NTU, KW;
+  int MT, BPX, KS, U, NT, TPW, NTU, KW;
   bool ok;
 };
 
@@ -521,9 +536,12 @@ XShape xshape(int H, int B) {
   XShape x{};
   x.ok = false;
   if (H % 64 != 0 || B > 256 || B < 1) return x;
-  x.MT = B > 128 ? 2 : 1;
+  const char* e = getenv("AM_XCD_BLOCKS");
+  const bool one = e && e[0] == '1' && e[1] == 0;
+  x.MT = B > 128 && one ? 2 : 1;
+  x.BPX = B > 128 && !one ? 2 : 1;
   x.KS = H / 32;
-  x.U = xcd_units(H);
+  x.U = xcd_units(H, 32 / x.BPX);
   if (x.U == 0) return x;
   x.NT = x.U / 4;
   x.TPW = (x.MT * x.NT + 3) / 4;
@@ -531,7 +549,7 @@ XShape xshape(int H, int B) {
   x.KW = 4 * H / 32 / 8;  // backward k-steps per wave (eight waves)
   // resident weight fragments per wave (4 VGPRs each): forward TPW x KS/2,
   // backward KW x NTU
-  x.ok = x.TPW * x.KS / 2 <= 36 && x.KW * x.NTU <= 24 && x.TPW <= 3 && x.NTU <= 2;
+  x.ok = x.TPW * x.KS / 2 <= 36 && x.KW * x.NTU <= 36 && x.TPW <= 3 && x.NTU <= 3;
   return x;
 }
 
@@ -546,11 +564,12 @@ hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipS
   const XShape x = xshape(a.hidden, ps.B);
   if (!x.ok) return hipSuccess;
   y.units = x.U;
-  const int blocks = NX * (a.hidden / x.U);
+  const int blocks = NX * x.BPX * (a.hidden / x.U);
   const size_t lds = (size_t)16 * x.MT * x.KS * 64 + 2 * 8 * x.TPW * 64 * 16;
   void* args[] = {&a, &ps, &y};
-  // instantiated shapes: H = 768 (B <= 128 and <= 256), H = 64, 128
-  AM_FWD_CASE(2, 24, 3) AM_FWD_CASE(1, 24, 2)
+  // instantiated shapes: H = 768 (B <= 128, B <= 256 in blocks of 16 or 32),
+  // H = 64, 128
+  AM_FWD_CASE(1, 24, 3) AM_FWD_CASE(2, 24, 3) AM_FWD_CASE(1, 24, 2)
   AM_FWD_CASE(2, 2, 1) AM_FWD_CASE(1, 2, 1)
   AM_FWD_CASE(2, 4, 1) AM_FWD_CASE(1, 4, 1)
   return hipSuccess;
@@ -565,14 +584,14 @@ hipError_t lstm_bwd_xcd_launch(PersistBwd a, PersistSchedule ps, XcdSync y, hipS
   const XShape x = xshape(a.hidden, ps.B);
   if (!x.ok) return hipSuccess;
   y.units = x.U;
-  const int blocks = NX * (a.hidden / x.U);
+  const int blocks = NX * x.BPX * (a.hidden / x.U);
   // two private chunk buffers per wave, or the partial products if larger
   const int ch = x.KW >= 4 ? 4 : x.KW;
   const size_t chunks = (size_t)8 * 2 * 16 * x.MT * ch * 64;
   const size_t red = (size_t)8 * x.MT * x.NTU * 64 * 16;
   const size_t lds = chunks > red ? chunks : red;
   void* args[] = {&a, &ps, &y};
-  AM_BWD_CASE(2, 2, 12) AM_BWD_CASE(1, 2, 12)
+  AM_BWD_CASE(1, 3, 12) AM_BWD_CASE(2, 2, 12) AM_BWD_CASE(1, 2, 12)
   AM_BWD_CASE(2, 1, 1) AM_BWD_CASE(1, 1, 1)
   AM_BWD_CASE(2, 1, 2) AM_BWD_CASE(1, 1, 2)
   return hipSuccess;
@@ -582,9 +601,10 @@ bool lstm_xcd_instantiated(bool forward, int hidden, int B) {
   const XShape x = xshape(hidden, B);
   if (!x.ok) return false;
   if (forward)
-    return (x.KS == 24 && ((x.MT == 2 && x.TPW == 3) || (x.MT == 1 && x.TPW == 2))) ||
+    return (x.KS == 24 && ((x.MT == 2 && x.TPW == 3) || (x.MT == 1 && (x.TPW == 2 || x.TPW == 3)))) ||
            ((x.KS == 2 || x.KS == 4) && x.TPW == 1);
-  return (x.KW == 12 && x.NTU == 2) || ((x.KW == 1 || x.KW == 2) && x.NTU == 1);
+  return (x.KW == 12 && (x.NTU == 2 || (x.MT == 1 && x.NTU == 3))) ||
+         ((x.KW == 1 || x.KW == 2) && x.NTU == 1);
 }
 
 }  // namespace am

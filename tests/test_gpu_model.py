@@ -108,6 +108,28 @@ def test_bf16_small_matches_oracle(lengths_kind):
     say(f"  max rel err {max(errs.values()):.2e}")
 
 
+@pytest.mark.parametrize("blocks", ["pairs", "single"])
+def test_bf16_wide_batch_block_layouts(blocks, monkeypatch):
+    # 200 sequences (> 128): by default blocks of 16 sequences, two per XCD
+    # (13 blocks, the last one half full); AM_XCD_BLOCKS=1 selects blocks of
+    # 32, one per XCD.  Varying lengths end blocks at different steps.
+    if blocks == "single":
+        monkeypatch.setenv("AM_XCD_BLOCKS", "1")
+    else:
+        monkeypatch.delenv("AM_XCD_BLOCKS", raising=False)
+    dims = oracle.ModelDims(2, 64, 128, 520)
+    T, B = 6, 200
+    lengths = np.sort(np.random.default_rng(8).integers(1, T + 1, B))[::-1].astype(np.int32)
+    lengths[0] = T
+    say(f"bf16 wide batch, {blocks}")
+    master, x, idx, prob, h0, c0 = _problem(dims, T, B, 8, 0.98, lengths, seed=17, state=True)
+    m = am.Model(dims.layers, dims.input_dim, dims.hidden, dims.classes, am.BF16)
+    got = gpu_forward_backward(m, master, x, T, B, idx, prob, lengths, h0, c0, want_state=True)
+    ref = oracle_forward_backward(dims, master, x, T, B, idx, prob, lengths, h0, c0, bf16=True)
+    errs = _check(got, ref, dims, BF16_TOL, state=True)
+    say(f"  max rel err {max(errs.values()):.2e}")
+
+
 def test_runs_are_bitwise_deterministic():
     dims = oracle.ModelDims(2, 64, 128, 520)
     T, B = 9, 130
