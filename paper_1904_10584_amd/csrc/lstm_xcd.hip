@@ -20,9 +20,9 @@
 // A workgroup owns U hidden units (U % 4 == 0) of one block of RB sequences
 // (RB = 16 or 32).  The forward product keeps the workgroup's 4U columns of
 // W_h resident in registers in unit-major, gate-minor order, so a 16-column
-// MFMA tile holds 4 units x 4 gates; a per-wave transpose of 4x4 quads
-// through LDS then gives each lane all four gate pre-activations of one
-// (sequence, unit).  The backward product keeps the U columns of W_h in
+// MFMA tile holds 4 units x 4 gates; reading the partial tiles back from
+// LDS in 4x4-quad-transposed order then gives each lane all four gate
+// pre-activations of one (sequence, unit).  The backward product keeps the U columns of W_h in
 // registers too.
 #include <cstdlib>
 
@@ -130,8 +130,8 @@ __device__ __forceinline__ int active_up(const PersistSchedule& ps, int nb, int 
 // the whole launch.  Each step the block's rows of h_{t-1} are copied to
 // LDS with direct loads (whole 128-byte lines), laid out line-major
 // [H/64 lines][RB rows][128 B] with the 16-byte chunks of a row XOR-swizzled
-// by row, and read back as MFMA fragments.  The two k-halves of a group swap
-// partial tiles through LDS: the k-half-0 wave finishes the first
+// by row, and read back as MFMA fragments.  The two k-halves of a group
+// publish their partial tiles to LDS: the k-half-0 wave finishes the first
 // ceil(TPW/2) tiles, the k-half-1 wave the rest.  A step is signalled as soon
 // as its h stores (the only exchanged data) are complete; the cell state,
 // gate and h_{t-1} copies are stored after the signal.
@@ -145,7 +145,6 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
   extern __shared__ __align__(16) unsigned char lds[];
   bf16_t* hl = reinterpret_cast<bf16_t*>(lds);
   f32x4_t* red = reinterpret_cast<f32x4_t*>(lds + HS_BYTES);  // [8][TPW][64]
-  f32x4_t* xs = red + 8 * TPW * 64;                             // [8][TPW][64]
   __shared__ int bad_sh;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -156,7 +155,6 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
   const int blk = xcd_block(members), us = (blockIdx.x / NX) % members;
   const int b0 = blk * RB, j0 = us * U;
   const int mw = g % MT;
-  const int ts_lo = kh == 0 ? 0 : FIN, ts_hi = kh == 0 ? FIN : TPW;
   const bf16_t* __restrict__ P = static_cast<const bf16_t*>(a.P);
   const bf16_t* __restrict__ Wh = static_cast<const bf16_t*>(a.Wh);
   const bf16_t* __restrict__ h0 = static_cast<const bf16_t*>(a.h0);
@@ -254,30 +252,23 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
       }
     }
 
-    // the k-halves of the group swap the partial tiles the other finishes
+    // both k-halves publish all their partial tiles; each lane then reads
+    // the two partials of its cells straight in transposed order (4x4 quads:
+    // lane l takes, for row 4(l/16) + l%4, the 4 gates of its unit from
+    // lanes (l & ~3) + q).  Selecting among the accumulators by the runtime
+    // k-half instead would index them dynamically: compare/select chains.
 #pragma unroll
-    for (int ts = 0; ts < TPW; ++ts)
-      if (!(ts >= ts_lo && ts < ts_hi)) red[(wave * TPW + ts) * 64 + lane] = acc[ts];
+    for (int ts = 0; ts < TPW; ++ts) red[(wave * TPW + ts) * 64 + lane] = acc[ts];
     __syncthreads();
-    f32x4_t fin[FIN];
-#pragma unroll
-    for (int o = 0; o < FIN; ++o) {
-      const int ts0 = o, ts1 = FIN + o < TPW ? FIN + o : o;  // static candidates
-      fin[o] = kh == 0 ? acc[ts0] : acc[ts1];
-      fin[o] += red[((wave ^ 4) * TPW + slot_ts(o) % TPW) * 64 + lane];
-    }
-
-    // 4x4 quad transpose: lane l gets, for row 4(l/16) + l%4, the 4 gates
-    // of its unit from lanes (l & ~3) + q
-    f32x4_t* xw = xs + wave * TPW * 64;
-#pragma unroll
-    for (int o = 0; o < FIN; ++o) xw[o * 64 + lane] = fin[o];
     float gate[FIN][4];
 #pragma unroll
-    for (int o = 0; o < FIN; ++o)
+    for (int o = 0; o < FIN; ++o) {
+      const int ts = slot_ts(o) % TPW;
+      const float* p0 = reinterpret_cast<const float*>(red + (g * TPW + ts) * 64 + (lane & ~3));
+      const float* p1 = reinterpret_cast<const float*>(red + ((g + 4) * TPW + ts) * 64 + (lane & ~3));
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        gate[o][q] = reinterpret_cast<const float*>(xw + o * 64 + (lane & ~3) + q)[lane & 3];
+      for (int q = 0; q < 4; ++q) gate[o][q] = p0[4 * q + (lane & 3)] + p1[4 * q + (lane & 3)];
+    }
 
     const int b = b0 + qrow;
     const bool row_ok = b < nb;
@@ -565,7 +556,7 @@ hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipS
   if (!x.ok) return hipSuccess;
   y.units = x.U;
   const int blocks = NX * x.BPX * (a.hidden / x.U);
-  const size_t lds = (size_t)16 * x.MT * x.KS * 64 + 2 * 8 * x.TPW * 64 * 16;
+  const size_t lds = (size_t)16 * x.MT * x.KS * 64 + 8 * x.TPW * 64 * 16;
   void* args[] = {&a, &ps, &y};
   // instantiated shapes: H = 768 (B <= 128, B <= 256 in blocks of 16 or 32),
   // H = 64, 128
