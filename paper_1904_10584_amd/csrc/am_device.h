@@ -31,6 +31,27 @@ template <typename T> __device__ __forceinline__ T from_f32(float v);
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
 
+// Saved gate activations of a row: unit j's four gates (i, f, g, o) sit
+// together at 4j .. 4j+3, so one cell's gates move as one 8-byte (bf16) or
+// 16-byte (fp32) access.
+__device__ __forceinline__ void store_gates(bf16_t* grow, int j, float i, float f, float g, float o) {
+  *reinterpret_cast<uint2*>(grow + 4 * j) =
+      make_uint2((uint32_t)f32_to_bf16(i) | ((uint32_t)f32_to_bf16(f) << 16),
+                 (uint32_t)f32_to_bf16(g) | ((uint32_t)f32_to_bf16(o) << 16));
+}
+__device__ __forceinline__ void store_gates(float* grow, int j, float i, float f, float g, float o) {
+  *reinterpret_cast<float4*>(grow + 4 * j) = make_float4(i, f, g, o);
+}
+__device__ __forceinline__ void load_gates(const bf16_t* grow, int j, bf16_t (&v)[4]) {
+  const uint2 u = *reinterpret_cast<const uint2*>(grow + 4 * j);
+  v[0] = (bf16_t)(u.x & 0xFFFFu); v[1] = (bf16_t)(u.x >> 16);
+  v[2] = (bf16_t)(u.y & 0xFFFFu); v[3] = (bf16_t)(u.y >> 16);
+}
+__device__ __forceinline__ void load_gates(const float* grow, int j, float (&v)[4]) {
+  const float4 u = *reinterpret_cast<const float4*>(grow + 4 * j);
+  v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+}
+
 // One MFMA operand fragment: 8 consecutive k-elements of one row (A) or one
 // column (B) of a 16x16 output tile.  Lane l serves row/column l % 16 and
 // the k-octet l / 16 of a 32-wide k-step.  The same k-octet mapping is used

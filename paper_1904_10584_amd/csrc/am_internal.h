@@ -48,7 +48,7 @@ struct LstmFwdStep {
   void* H;            // [nb][H] h_t (written)
   void* Hs;           // [nb][H] copy of h_{t-1} for the Wh gradient (written)
   float* C;           // [nb][H] c_t (written)
-  void* G;            // [nb][4H] gate activations i,f,g,o (written)
+  void* G;            // [nb][H][4] gate activations: unit j's i, f, g, o at 4j .. 4j+3 (written)
   int nb, hidden;
   bool bf16;
 };

@@ -210,11 +210,7 @@ __global__ __launch_bounds__(256, 1) void lstm_fwd_persist(PersistFwd a, Persist
       a.C[o] = c;
       Hb[o] = h;
       Hs[o] = h_reg[r];
-      T* grow = Gb + (int64_t)(off + b) * G4;
-      grow[j] = from_f32<T>(gi);
-      grow[H + j] = from_f32<T>(gf);
-      grow[2 * H + j] = from_f32<T>(gg);
-      grow[3 * H + j] = from_f32<T>(go);
+      store_gates(Gb + (int64_t)(off + b) * G4, j, gi, gf, gg, go);
       c_reg[r] = c;
       h_reg[r] = h;
     }
@@ -293,11 +289,12 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_persist(PersistBwd a, Persist
     for (int q = 0; q < 2; ++q) {
       const int b = min(b0 + tile * 16 + mfma_row(lane, 2 * rpair + q), nb - 1);
       const int64_t o = (int64_t)(off + b) * H + j;
-      const T* grow = Gb + (int64_t)(off + b) * G4;
-      gi[q] = grow[j];
-      gf[q] = grow[H + j];
-      gg[q] = grow[2 * H + j];
-      go[q] = grow[3 * H + j];
+      T gq[4];
+      load_gates(Gb + (int64_t)(off + b) * G4, j, gq);
+      gi[q] = gq[0];
+      gf[q] = gq[1];
+      gg[q] = gq[2];
+      go[q] = gq[3];
       cc[q] = a.C[o];
       cp[q] = cprev_rows[(int64_t)b * H + j];
       dh[q] = dHa[o];

@@ -125,11 +125,7 @@ __global__ __launch_bounds__(256) void lstm_fwd_step_kernel(
     Cout[o] = c;
     Hout[o] = from_f32<T>(h);
     Hs[o] = hp[r];
-    T* grow = G + (int64_t)row * G4;
-    grow[j] = from_f32<T>(gi);
-    grow[H + j] = from_f32<T>(gf);
-    grow[2 * H + j] = from_f32<T>(gg);
-    grow[3 * H + j] = from_f32<T>(go);
+    store_gates(G + (int64_t)row * G4, j, gi, gf, gg, go);
   }
 }
 
@@ -161,9 +157,7 @@ __global__ __launch_bounds__(256) void lstm_bwd_step_kernel(
     const int row0 = b0 + wave * 16 + mfma_row(lane, r);
     const int row = min(row0, nb - 1);
     const int64_t o = (int64_t)row * H + j;
-    const T* grow = G + (int64_t)row * G4;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) gv[r][g] = grow[g * H + j];
+    load_gates(G + (int64_t)row * G4, j, gv[r]);
     cv[r] = C[o];
     cpv[r] = Cprev ? Cprev[o] : 0.f;
     dcv[r] = dc[o];  // used only where the sequence continues to t+1

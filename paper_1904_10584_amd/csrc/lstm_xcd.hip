@@ -83,12 +83,15 @@ __device__ __forceinline__ void xsignal(const XcdSync& y, bool local, int blk) {
   }
 }
 
-// Wait until the block's counter reaches `target` (members x steps).  One
-// lane polls with device-scope loads, which bypass the CU's L1; the other
+// Wait until the block's counter reaches `target` (members x steps).  Thread
+// `poller` polls with device-scope loads, which bypass the CU's L1; the other
 // workgroups' exchanged rows are then read from the shared L2 (local) or
 // after an acquire that invalidates this CU's caches (block spans XCDs).
-__device__ __forceinline__ void xwait(const XcdSync& y, bool local, int blk, unsigned target) {
-  if (threadIdx.x == 0) {
+// Each poll waits for every load its wave has in flight, so the poller
+// should belong to a wave with none outstanding.
+__device__ __forceinline__ void xwait(const XcdSync& y, bool local, int blk, unsigned target,
+                                      int poller = 0) {
+  if (threadIdx.x == poller) {
     const unsigned* cnt = y.flags + blk * 32;
     unsigned spins = 0;
     while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
@@ -298,9 +301,7 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
       const int64_t ofs = (int64_t)(off + b) * H + j;
       a.C[ofs] = cnew[o];
       Hs[ofs] = hprev[o];
-      bf16_t* grow = Gb + (int64_t)(off + b) * G4;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) grow[q * H + j] = f32_to_bf16(gate[o][q]);
+      store_gates(Gb + (int64_t)(off + b) * G4, j, gate[o][0], gate[o][1], gate[o][2], gate[o][3]);
     }
     off_prev = off;
     off += nb;
@@ -327,6 +328,7 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
   constexpr int CHB = RB * CH * 64;           // bytes per chunk
   constexpr int IPC = CHB / 1024;             // direct loads per chunk
   static_assert(KW % CH == 0 && IPC >= 1, "chunking");
+  static_assert(MT * NTU < 8, "the last wave finishes no tile (it polls the barrier)");
   extern __shared__ __align__(16) unsigned char lds[];
   bf16_t* buf = reinterpret_cast<bf16_t*>(lds + (threadIdx.x >> 6) * 2 * CHB);
   f32x4_t* red = reinterpret_cast<f32x4_t*>(lds);  // [8][MT][NTU][64], after the products
@@ -387,9 +389,7 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
       for (int r = 0; r < 4; ++r) {
         const int b = min(b0 + fm * 16 + mfma_row(lane, r), nb - 1);
         const int64_t o = (int64_t)(off + b) * H + j;
-        const bf16_t* grow = Gb + (int64_t)(off + b) * G4;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) gv[r][q] = grow[q * H + j];
+        load_gates(Gb + (int64_t)(off + b) * G4, j, gv[r]);
         cv[r] = a.C[o];
         cpv[r] = cprev_rows[(int64_t)b * H + j];
         dhv[r] = dHa[o];
@@ -402,7 +402,8 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
 #pragma unroll
       for (int n = 0; n < NTU; ++n) acc[m][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (b0 < nb_next) {
-      xwait(y, local, blk, (unsigned)members * done);
+      // polled from the last wave, which has no cell-input loads in flight
+      xwait(y, local, blk, (unsigned)members * done, 64 * 7);
       const bf16_t* dAn = dA + (int64_t)off_next * G4 + wave * KW * 32;
       // chunk c of this wave's k-slice into buffer bi: RB rows x CH k-steps;
       // instruction i covers rows i*(64/CPR) .., 16-byte pieces swizzled by row
