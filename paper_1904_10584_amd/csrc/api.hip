@@ -197,7 +197,7 @@ constexpr int64_t SYNC_STICKY_WORD = SYNC_BYTES / 4 - 1;
 am::XcdSync xcd_sync(void* base) {
   unsigned* u = static_cast<unsigned*>(base);
   am::XcdSync y;
-  y.flags = u;             // counter of block k < 16 at u[32 k]
+  y.flags = u;             // flag line of block k < 16: u[32 k .. 32 k + 31], a word per member
   y.start = u + 512;
   y.err = reinterpret_cast<int*>(u + SYNC_STICKY_WORD);
   y.xcc = reinterpret_cast<int*>(u + 516);  // up to 1024 workgroups

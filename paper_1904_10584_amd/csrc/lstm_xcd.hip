@@ -12,9 +12,10 @@
 //     round-robin); at start every workgroup records its
 //     XCC id and, unless every block really is on one XCD, the kernel falls
 //     back to device-scope release/acquire for its whole run;
-//   * the step barrier is one counter per block, bumped with an atomic add
-//     by every member after its stores of the step have completed and
-//     polled by one lane with device-scope loads;
+//   * the step barrier is one 128-byte flag line per block: every member
+//     stores its count of completed steps in its own word once its stores
+//     of the step have completed, and one wave polls the line with
+//     device-scope loads;
 //   * every exchanged row is written once and read only after it was written,
 //     so no consumer's L1 can hold a stale copy.
 // A workgroup owns U hidden units (U % 4 == 0) of one block of RB sequences
@@ -68,35 +69,44 @@ __device__ bool check_local(const XcdSync& y, int* bad_sh) {
   return *bad_sh == 0;
 }
 
-// This workgroup's stores of the step have completed; count it in its
-// block's step counter.  Relaxed atomics are performed beyond the CU (in L2
-// or the memory side), so counter updates are seen by every poller; the
-// release fence (a write-back of this XCD's L2) is needed only when a block
-// spans XCDs.
-__device__ __forceinline__ void xsignal(const XcdSync& y, bool local, int blk) {
+// This workgroup's stores of the step have completed: publish its count of
+// completed steps in its own word of the block's flag line (one 128-byte
+// line of 32 words, word us for member us).  The device-scope store reaches
+// the XCD's L2 after the data stores it follows have completed there, so a
+// poller that sees the count then reads the data from L2; the release fence
+// (a write-back of this XCD's L2) is needed only when a block spans XCDs.
+// Separate words need no atomic read-modify-write, which the L2 would
+// serialise over the block's members.
+__device__ __forceinline__ void xsignal(const XcdSync& y, bool local, int blk, int us,
+                                        unsigned count) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
-    unsigned* cnt = y.flags + blk * 32;
     if (!local) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(y.flags + blk * 32 + us, count, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
-// Wait until the block's counter reaches `target` (members x steps).  Thread
-// `poller` polls with device-scope loads, which bypass the CU's L1; the other
-// workgroups' exchanged rows are then read from the shared L2 (local) or
-// after an acquire that invalidates this CU's caches (block spans XCDs).
-// Each poll waits for every load its wave has in flight, so the poller
-// should belong to a wave with none outstanding.
-__device__ __forceinline__ void xwait(const XcdSync& y, bool local, int blk, unsigned target,
-                                      int poller = 0) {
-  if (threadIdx.x == poller) {
-    const unsigned* cnt = y.flags + blk * 32;
+// Wait until every member of the block has published a count >= target.
+// Wave `poller` polls: lane m < members reads member m's word with a
+// device-scope load (bypassing the CU's L1; one request for the line) and
+// the wave votes.  The other workgroups' exchanged rows are then read from
+// the shared L2 (local) or after an acquire that invalidates this CU's
+// caches (block spans XCDs).  Each poll waits for every load its wave has
+// in flight, so the poller should be a wave with none outstanding.
+__device__ __forceinline__ void xwait(const XcdSync& y, bool local, int blk, int members,
+                                      unsigned target, int poller = 0) {
+  if ((int)(threadIdx.x >> 6) == poller) {
+    const int lane = threadIdx.x & 63;
+    const unsigned* line = y.flags + blk * 32;
     unsigned spins = 0;
-    while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+    for (;;) {
+      const unsigned v = lane < members
+                             ? __hip_atomic_load(line + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                             : target;
+      if (__all(v >= target)) break;
       if (++spins > SPIN_LIMIT) {
-        __hip_atomic_store(y.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (lane == 0) __hip_atomic_store(y.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;
       }
       __builtin_amdgcn_s_sleep(1);
@@ -217,7 +227,7 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
     for (int ts = 0; ts < TPW; ++ts) acc[ts] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     const bf16_t* hsrc = h0;
     if (t > 0) {
-      xwait(y, local, blk, (unsigned)(members * t));
+      xwait(y, local, blk, members, (unsigned)t);
       hsrc = Hb + (int64_t)off_prev * H;
     }
     if (hsrc) {
@@ -292,7 +302,7 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
         h_reg[o] = h;
       }
     }
-    xsignal(y, local, blk);  // h stores complete; its barrier also orders the LDS reuse
+    xsignal(y, local, blk, us, (unsigned)(t + 1));  // h stores complete; its barrier also orders the LDS reuse
     // stores only the backward pass reads
 #pragma unroll
     for (int o = 0; o < FIN; ++o) {
@@ -403,7 +413,7 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
       for (int n = 0; n < NTU; ++n) acc[m][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (b0 < nb_next) {
       // polled from the last wave, which has no cell-input loads in flight
-      xwait(y, local, blk, (unsigned)members * done, 64 * 7);
+      xwait(y, local, blk, members, done, 7);
       const bf16_t* dAn = dA + (int64_t)off_next * G4 + wave * KW * 32;
       // chunk c of this wave's k-slice into buffer bi: RB rows x CH k-steps;
       // instruction i covers rows i*(64/CPR) .., 16-byte pieces swizzled by row
@@ -474,8 +484,8 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
       arow[2 * H + j] = f32_to_bf16(d_g * (1.f - vg * vg));
       arow[3 * H + j] = f32_to_bf16(d_o * vo * (1.f - vo));
     }
-    xsignal(y, local, blk);  // its barrier also orders the LDS reuse
     ++done;
+    xsignal(y, local, blk, us, done);  // its barrier also orders the LDS reuse
   }
 }
 
