@@ -326,8 +326,9 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
 // fetches its k-slice of the block's dA_{t+1} rows itself, with direct loads
 // into two private LDS buffers in chunks of CH k-steps, so it waits only on
 // its own loads.  The eight partial products are summed in a fixed order
-// through LDS, and waves f < MT NTU finish tile (row tile f % MT, unit tile
-// f / MT): the cell backward, with dc carried in registers.
+// through LDS; the cell backward (dc carried in registers) is spread over
+// the first seven waves in items of one row per lane, an equal number per
+// SIMD, while the last wave polls the step barrier.
 template <int MT, int NTU, int KW>
 __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSchedule ps, XcdSync y) {
   constexpr int RB = 16 * MT;                 // sequences per block
@@ -338,7 +339,7 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
   constexpr int CHB = RB * CH * 64;           // bytes per chunk
   constexpr int IPC = CHB / 1024;             // direct loads per chunk
   static_assert(KW % CH == 0 && IPC >= 1, "chunking");
-  static_assert(MT * NTU < 8, "the last wave finishes no tile (it polls the barrier)");
+  static_assert(MT * NTU * 4 <= 32, "cell items: at most 8 per SIMD");
   extern __shared__ __align__(16) unsigned char lds[];
   bf16_t* buf = reinterpret_cast<bf16_t*>(lds + (threadIdx.x >> 6) * 2 * CHB);
   f32x4_t* red = reinterpret_cast<f32x4_t*>(lds);  // [8][MT][NTU][64], after the products
@@ -367,13 +368,26 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
   }
   const bool local = check_local(y, &bad_sh);
 
-  // finishing tile of this wave (waves f < MT NTU)
-  const int fm = wave % MT, fn = wave / MT;
-  const bool fin = wave < MT * NTU;
-  const int uu = 16 * (fin ? fn : 0) + (lane & 15);  // unit within the slice
-  const bool uok = fin && uu < U;
-  const int j = j0 + (uok ? uu : 0);
-  float dc_reg[4] = {0.f, 0.f, 0.f, 0.f};
+  // Cell work: items p = (row tile m, unit tile n, quad row r), MT NTU 4 of
+  // them; item p covers, per lane, unit 16n + lane%16 and row
+  // 16m + 4(lane/16) + r.  Each SIMD (waves s and s+4) takes IPS consecutive
+  // items, its first wave the first half; the last wave polls the barrier
+  // and takes none, so wave 3 takes all of SIMD 3's.
+  constexpr int NI = MT * NTU * 4, IPS = (NI + 3) / 4;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);  // (scalar: the item indices are wave-uniform)
+  const int simd = wv & 3, s_lo = min(NI, simd * IPS), s_hi = min(NI, s_lo + IPS);
+  const int s_mid = simd == 3 ? s_hi : min(s_hi, s_lo + (IPS + 1) / 2);
+  const int i_lo = wv < 4 ? s_lo : s_mid, i_hi = wv < 4 ? s_mid : (wv == 7 ? s_mid : s_hi);
+  const int nitems = i_hi - i_lo;  // at most IPS
+  auto item_m = [&](int k) { return (i_lo + k) / (NTU * 4); };
+  auto item_n = [&](int k) { return ((i_lo + k) / 4) % NTU; };
+  auto item_r = [&](int k) { return (i_lo + k) % 4; };
+  auto item_u = [&](int k) { return 16 * item_n(k) + (lane & 15); };  // unit within the slice
+  auto item_j = [&](int k) { return j0 + (item_u(k) < U ? item_u(k) : 0); };
+  auto item_row = [&](int k) { return item_m(k) * 16 + mfma_row(lane, item_r(k)); };
+  float dc_reg[IPS];
+#pragma unroll
+  for (int k = 0; k < IPS; ++k) dc_reg[k] = 0.f;
 
   int nb = ps.T > 0 ? active_up(ps, 0, ps.T - 1) : 0;
   int off = ps.N - nb;
@@ -390,19 +404,20 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
     const int nb_prev = t > 0 ? active_up(ps, nb, t - 1) : 0;
     const int off_prev = off - nb_prev;
 
-    // the finishing waves' cell inputs (independent of the exchange)
-    bf16_t gv[4][4], dhv[4];
-    float cv[4], cpv[4];
-    if (fin) {
+    // this wave's cell inputs (independent of the exchange)
+    bf16_t gv[IPS][4], dhv[IPS];
+    float cv[IPS], cpv[IPS];
+    {
       const float* cprev_rows = t > 0 ? a.C + (int64_t)off_prev * H : a.c0;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int b = min(b0 + fm * 16 + mfma_row(lane, r), nb - 1);
+      for (int k = 0; k < IPS; ++k) {
+        if (k >= nitems) break;  // (wave-uniform)
+        const int b = min(b0 + item_row(k), nb - 1), j = item_j(k);
         const int64_t o = (int64_t)(off + b) * H + j;
-        load_gates(Gb + (int64_t)(off + b) * G4, j, gv[r]);
-        cv[r] = a.C[o];
-        cpv[r] = cprev_rows[(int64_t)b * H + j];
-        dhv[r] = dHa[o];
+        load_gates(Gb + (int64_t)(off + b) * G4, j, gv[k]);
+        cv[k] = a.C[o];
+        cpv[k] = cprev_rows[(int64_t)b * H + j];
+        dhv[k] = dHa[o];
       }
     }
 
@@ -412,7 +427,7 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
 #pragma unroll
       for (int n = 0; n < NTU; ++n) acc[m][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (b0 < nb_next) {
-      // polled from the last wave, which has no cell-input loads in flight
+      // polled from the last wave, which has no cell work and no loads in flight
       xwait(y, local, blk, members, done, 7);
       const bf16_t* dAn = dA + (int64_t)off_next * G4 + wave * KW * 32;
       // chunk c of this wave's k-slice into buffer bi: RB rows x CH k-steps;
@@ -459,25 +474,26 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
 #pragma unroll
       for (int n = 0; n < NTU; ++n) red[((wave * MT + m) * NTU + n) * 64 + lane] = acc[m][n];
     __syncthreads();
-    f32x4_t rec = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    if (fin) {
-#pragma unroll
-      for (int w = 0; w < 8; ++w) rec += red[((w * MT + fm) * NTU + fn) * 64 + lane];
-    }
 
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int b = b0 + fm * 16 + mfma_row(lane, r);
-      if (!uok || b >= nb) continue;
+    for (int k = 0; k < IPS; ++k) {
+      if (k >= nitems) break;  // (wave-uniform)
+      // the eight partial products of this item's cell, in wave order
+      const int m = item_m(k), n = item_n(k), r = item_r(k);
+      float rec = 0.f;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) rec += reinterpret_cast<const float*>(red + ((w * MT + m) * NTU + n) * 64 + lane)[r];
+      const int b = b0 + item_row(k), j = item_j(k);
+      if (item_u(k) >= U || b >= nb) continue;
       const bool cont = b < nb_next;
-      const float vi = bf16_to_f32(gv[r][0]), vf = bf16_to_f32(gv[r][1]);
-      const float vg = bf16_to_f32(gv[r][2]), vo = bf16_to_f32(gv[r][3]);
-      const float dhh = bf16_to_f32(dhv[r]) + (cont ? rec[r] : 0.f);
-      const float tc = tanh_f(cv[r]);
+      const float vi = bf16_to_f32(gv[k][0]), vf = bf16_to_f32(gv[k][1]);
+      const float vg = bf16_to_f32(gv[k][2]), vo = bf16_to_f32(gv[k][3]);
+      const float dhh = bf16_to_f32(dhv[k]) + (cont ? rec : 0.f);
+      const float tc = tanh_f(cv[k]);
       const float d_o = dhh * tc;
-      const float dcell = dhh * vo * (1.f - tc * tc) + (cont ? dc_reg[r] : 0.f);
-      const float d_i = dcell * vg, d_g = dcell * vi, d_f = dcell * cpv[r];
-      dc_reg[r] = dcell * vf;
+      const float dcell = dhh * vo * (1.f - tc * tc) + (cont ? dc_reg[k] : 0.f);
+      const float d_i = dcell * vg, d_g = dcell * vi, d_f = dcell * cpv[k];
+      dc_reg[k] = dcell * vf;
       bf16_t* arow = dA + (int64_t)(off + b) * G4;
       arow[j] = f32_to_bf16(d_i * vi * (1.f - vi));
       arow[H + j] = f32_to_bf16(d_f * vf * (1.f - vf));
