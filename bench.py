@@ -37,8 +37,9 @@ def parse():
     ap.add_argument("--workload", default="paper-5x768")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-worker-kernels", action="store_true",
-                    help="skip timing the side kernels (BMUF step, 8-stream aggregate, input features, "
-                         "target delay, teacher target generation)")
+                    help="skip timing the side kernels (the step's HBM-bound kernels in and out of "
+                         "cache, BMUF step, 8-stream aggregate, input features, target delay, teacher "
+                         "target generation)")
     ap.add_argument("--cpu-chunks", type=int, default=0,
                     help="chunks the CPU oracle runs forward/backward on (0 = the whole batch)")
     return ap.parse_args()
@@ -170,6 +171,73 @@ def worker_kernels(am, n, reps):
     # algorithmic bytes: every word read once, the dense update written once
     kt = dict(kt, bytes=(4.0 * n + 4.0 * total_words) * kt["launches"])
     out["decode_multi"] = dict(_hbm_entry(kt, reps), streams=S, words=total_words)
+    return out
+
+
+def hbm_kernels(am, synth, w, n, reps):
+    """The step's HBM-bound kernels at the step's sizes, each timed two ways
+    (HIP events around the library's launches): in a loop over the same
+    buffers, and with a 1 GiB read of another buffer between launches so that
+    their inputs come from HBM, not from the 256 MB Infinity Cache or the
+    L2s (a read leaves those caches clean; a write would leave dirty lines
+    whose write-back the timed kernel would pay).
+    Algorithmic bytes: soft-target CE reads the fp32 logits and the k
+    (index, probability) pairs and writes bf16 dlogits; the encoder reads g
+    and r, writes r and the 2-bit codes' words (12 B per element + 4 B per
+    emitted word); the decoder writes the dense update and reads the words
+    (4 B per element + 4 B per word); SGD reads the master and the update
+    and writes the master and its bf16 copy (14 B per element)."""
+    import torch
+    dev = torch.device("cuda")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(8)
+    flush = torch.zeros(1 << 28, device=dev)  # 1 GiB
+
+    def timed(cls, launch, extra_bytes=lambda: 0.0):
+        res = {}
+        for mode in ("in_loop", "flushed"):
+            launch()
+            torch.cuda.synchronize()
+            extra = 0.0
+            am.profile_begin([cls])
+            for i in range(reps):
+                if mode == "flushed":
+                    flush.sum()
+                launch()
+                extra += extra_bytes()
+            am.profile_end()
+            kt = am.profile_get(cls)
+            res[mode] = _hbm_entry(dict(kt, bytes=kt["bytes"] + extra), reps)
+        return res
+
+    out = {}
+    N, C, K = w["T"] * w["B"], w["classes"], w["K"]
+    idx_np, prob_np = synth.teacher_targets(N, C, K, w["mass"])
+    idx = torch.from_numpy(idx_np).to(dev)
+    prob = torch.from_numpy(prob_np).to(dev)
+    z = torch.randn((N, C), generator=gen, device=dev) * 3.0
+    dz = torch.empty((N, C), dtype=torch.bfloat16, device=dev)
+    loss = torch.zeros(1, device=dev)
+    cws = torch.empty(am.ce_workspace_bytes(N), dtype=torch.uint8, device=dev)
+    out["soft_ce"] = dict(timed(am.K_CE, lambda: am.sparse_soft_ce(z, idx, prob, loss, dz, cws)),
+                          frames=N, classes=C, k=K)
+    del z, dz, idx, prob
+    tau = w["tau"]
+    g = torch.randn(n, generator=gen, device=dev) * 1e-3
+    r = torch.zeros(n, device=dev)
+    words = torch.zeros(n, dtype=torch.int32, device=dev)
+    count = torch.zeros(1, dtype=torch.int64, device=dev)
+    ews = torch.zeros(am.encode_workspace_bytes(n), dtype=torch.uint8, device=dev)
+    word_bytes = lambda: 4.0 * float(count.item())  # read after each launch's count
+    out["encode"] = dict(timed(am.K_ENCODE, lambda: am.grad_threshold_encode(g, r, tau, words, count, ews),
+                               word_bytes), elements=n, words_last=int(count.item()))
+    dense = torch.empty(n, device=dev)
+    out["decode"] = dict(timed(am.K_DECODE, lambda: am.grad_threshold_decode(words, count, tau, dense),
+                               word_bytes), elements=n, words=int(count.item()))
+    master = torch.randn(n, generator=gen, device=dev) * 0.03
+    wbf = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    out["sgd"] = dict(timed(am.K_SGD, lambda: am.sgd_apply(master, g, 1e-6, wbf)), elements=n)
+    del flush
     return out
 
 
@@ -375,6 +443,7 @@ def main():
                                if totals[k]["launches"] > 0},
     }
     if not args.no_worker_kernels:
+        out["hbm_kernels"] = hbm_kernels(am, synth, w, st.n, reps=10)
         out["worker_kernels"] = worker_kernels(am, st.n, reps=10)
         if lengths is None:
             out["input_kernels"] = input_kernels(am, synth, w, N, reps=10)

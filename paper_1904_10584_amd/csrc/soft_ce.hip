@@ -2,7 +2,8 @@
 // teacher's k-best posteriors), HBM-bound.
 //
 // One wave per frame row: the row of logits is read once with 16-byte loads
-// and kept in registers (up to 8192 classes), max and sum-of-exponentials are
+// issued back to back and kept in registers (up to 8192 classes), max and
+// sum-of-exponentials are
 // wave reductions, the k teacher logits are read with wave-uniform loads, and
 // the gradient row  s (M softmax(z) - scatter(p))  is written once.  A teacher
 // entry is subtracted by the one lane that holds its class; which register
@@ -40,10 +41,28 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
   float row_loss = 0.f;
 
   if (f < N) {
-    const float m = mask ? (mask[f] != 0 ? 1.f : 0.f) : 1.f;
-    const float s = m * (scale_dev ? *scale_dev : scale_host);
     const float* zr = z + f * C;
     DT* dr = dz + f * C;
+    // the row first, 16-byte loads issued back to back (a lane past C
+    // re-reads the row's start; its values are replaced below), so that
+    // the row costs one memory latency, not one per chunk
+    float4 v[NCH];
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int c = i * 256 + lane * 4;
+      v[i] = *reinterpret_cast<const float4*>(zr + (c < C ? c : 0));
+    }
+    // teacher entries: lane j holds entry j (K <= 64 per pass)
+    const int32_t* ir = idx + f * K;
+    const float* pr = prob + f * K;
+    int tc = -1;
+    float tp = 0.f;
+    if (lane < K) {
+      tc = ir[lane];
+      tp = pr[lane];
+    }
+    const float m = mask ? (mask[f] != 0 ? 1.f : 0.f) : 1.f;
+    const float s = m * (scale_dev ? *scale_dev : scale_host);
     if (s == 0.f) {
 #pragma unroll
       for (int i = 0; i < NCH; ++i) {
@@ -51,35 +70,30 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
         if (c < C) store4<DT>(dr + c, make_float4(0.f, 0.f, 0.f, 0.f));
       }
     } else {
-      // teacher entries: lane j holds entry j (K <= 64 per pass); their
-      // loads overlap the row loads below
-      const int32_t* ir = idx + f * K;
-      const float* pr = prob + f * K;
-      int tc = -1;
-      float tp = 0.f, tz = 0.f;
-      if (lane < K) {
-        tc = ir[lane];
-        tp = pr[lane];
-        if (tc < 0 || tc >= C) { tc = -1; tp = 0.f; }  // empty slot (or out of range)
-        else tz = zr[tc];
-      }
-      float4 v[NCH];
+      // each entry's own logit (a lane's slot past K, an empty slot or an
+      // out-of-range index reads the row's first logit and is dropped);
+      // issued before the reductions below, which hide its latency
+      const bool tok = tc >= 0 && tc < C;
+      float tz = zr[tok ? tc : 0];
+      asm volatile("" ::: "memory");  // keep the load here, ahead of its use
+      if (!tok) { tc = -1; tp = 0.f; }
       float mx = -INFINITY;
 #pragma unroll
       for (int i = 0; i < NCH; ++i) {
-        const int c = i * 256 + lane * 4;
-        if (c < C) {
-          v[i] = *reinterpret_cast<const float4*>(zr + c);
-          mx = fmaxf(mx, fmaxf(fmaxf(v[i].x, v[i].y), fmaxf(v[i].z, v[i].w)));
-        } else {
-          v[i] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-        }
+        if (i * 256 + lane * 4 >= C) v[i] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+        mx = fmaxf(mx, fmaxf(fmaxf(v[i].x, v[i].y), fmaxf(v[i].z, v[i].w)));
       }
       mx = wave_max(mx);
+      // e = exp(z - max) kept in place of the row (0 past C)
       float se = 0.f;
 #pragma unroll
-      for (int i = 0; i < NCH; ++i)
-        se += __expf(v[i].x - mx) + __expf(v[i].y - mx) + __expf(v[i].z - mx) + __expf(v[i].w - mx);
+      for (int i = 0; i < NCH; ++i) {
+        v[i].x = __expf(v[i].x - mx);
+        v[i].y = __expf(v[i].y - mx);
+        v[i].z = __expf(v[i].z - mx);
+        v[i].w = __expf(v[i].w - mx);
+        se += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+      }
       se = wave_sum(se);
       const float lse = mx + __logf(se);
 
@@ -96,13 +110,14 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
       }
       mass = wave_sum(mass);
       lf = wave_sum(lf);
-      const float sm = s * mass;
+      // s M softmax(z) = e (s M / sum e)
+      const float sm = s * mass / se;
 #pragma unroll
       for (int i = 0; i < NCH; ++i) {
-        v[i].x = sm * __expf(v[i].x - lse);
-        v[i].y = sm * __expf(v[i].y - lse);
-        v[i].z = sm * __expf(v[i].z - lse);
-        v[i].w = sm * __expf(v[i].w - lse);
+        v[i].x *= sm;
+        v[i].y *= sm;
+        v[i].z *= sm;
+        v[i].w *= sm;
       }
       for (int jj = 0; jj < K; ++jj) {
         int c;
@@ -116,15 +131,24 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
           if (c >= C) c = -1;
         }
         if (c < 0) continue;
-        const int ci = c >> 8, owner = (c & 255) >> 2, cc = c & 3;
+        const int owner = (c & 255) >> 2, cc = c & 3;
         const float d = lane == owner ? s * p : 0.f;
+        // v[c / 256] component cc -= d, the chunk chosen with uniform tests
+        // on its group of four, then within the group (an index into the
+        // register array computed at run time would put it in scratch)
+        const int ci = c >> 8;
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-          if (i == ci) {  // wave-uniform
-            v[i].x -= cc == 0 ? d : 0.f;
-            v[i].y -= cc == 1 ? d : 0.f;
-            v[i].z -= cc == 2 ? d : 0.f;
-            v[i].w -= cc == 3 ? d : 0.f;
+        for (int g = 0; g < (NCH + 3) / 4; ++g) {
+          if (g == (ci >> 2)) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              if (4 * g + k < NCH && k == (ci & 3)) {
+                v[4 * g + k].x -= cc == 0 ? d : 0.f;
+                v[4 * g + k].y -= cc == 1 ? d : 0.f;
+                v[4 * g + k].z -= cc == 2 ? d : 0.f;
+                v[4 * g + k].w -= cc == 3 ? d : 0.f;
+              }
+            }
           }
         }
       }
