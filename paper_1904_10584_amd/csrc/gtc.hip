@@ -156,6 +156,27 @@ __device__ __forceinline__ int64_t lower_bound_words(const uint32_t* w, int64_t 
   return lo;
 }
 
+// The same, found by a whole wave: each round the 64 lanes probe 64 evenly
+// spaced positions of the remaining range [lo, hi] and a ballot of
+// (word < key), true on a prefix of the lanes, narrows it about 65-fold; the
+// last 64 or fewer candidates are tested at once.  About five rounds of
+// dependent loads for 2^24 words instead of 24.  Wave-uniform result.
+__device__ __forceinline__ int64_t lower_bound_wave(const uint32_t* w, int64_t cnt, uint32_t key,
+                                                    int lane) {
+  int64_t lo = 0, hi = cnt;  // the first word >= key lies in [lo, hi] (hi: none)
+  while (hi - lo > 64) {
+    const int64_t span = hi - lo;  // > 64, so the probes are strictly increasing
+    const int64_t p = lo + span * (lane + 1) / 65;
+    const int k = __popcll(__ballot(w[p] < key));  // probes 0 .. k-1 are below key
+    const int64_t below = lo + span * k / 65;          // probe k-1 (k >= 1)
+    const int64_t above = lo + span * (k + 1) / 65;    // probe k (k <= 63)
+    if (k > 0) lo = below + 1;
+    if (k < 64) hi = above;
+  }
+  const int64_t p = lo + lane;
+  return lo + __popcll(__ballot(p < hi && w[p] < key));
+}
+
 template <bool ACC>
 __global__ __launch_bounds__(TPB) void gtc_decode_tiles(const uint32_t* __restrict__ words,
                                                         const int64_t* __restrict__ count,
@@ -165,11 +186,13 @@ __global__ __launch_bounds__(TPB) void gtc_decode_tiles(const uint32_t* __restri
   __shared__ int64_t range[2];
   const int64_t base = (int64_t)blockIdx.x * TILE;
   const int64_t len = n - base < TILE ? n - base : TILE;
-  if (threadIdx.x < 2) {
+  if (threadIdx.x < 128) {  // wave 0: the tile's first word, wave 1: the next tile's
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
     int64_t cnt = *count;
     cnt = cnt < 0 ? 0 : (cnt > capacity ? capacity : cnt);
-    const int64_t end = base + (threadIdx.x ? len : 0);
-    range[threadIdx.x] = lower_bound_words(words, cnt, (uint32_t)(end << 1));
+    const int64_t end = base + (wv ? len : 0);
+    const int64_t r = lower_bound_wave(words, cnt, (uint32_t)(end << 1), lane);
+    if (lane == 0) range[wv] = r;
   }
   for (int i = threadIdx.x; i < TILE; i += TPB)
     tile[i] = (ACC && i < len) ? dense[base + i] : 0.f;
