@@ -41,17 +41,17 @@ namespace am {
 namespace {
 
 constexpr int BK = 64;    // k per tile
-constexpr int BM = 256;   // tile rows
+constexpr int BM0 = 256;  // tile rows (192 for some weight-gradient shapes)
 constexpr int NT = 512;   // threads per workgroup (8 waves: 2 x 4)
 constexpr int NW = 8;
 constexpr int NX = 8;     // XCDs
 
 __device__ uint4 g_zero[1];  // 16 zero bytes (the source of out-of-range chunks)
 
-template <int BN> struct Cfg {
+template <int BN, int BM> struct Cfg {
   static constexpr int WM = BM / 2;            // wave tile rows
   static constexpr int WN = BN / 4;            // wave tile columns
-  static constexpr int MI = WM / 16;           // 8
+  static constexpr int MI = WM / 16;           // 8 or 6
   static constexpr int NJ = WN / 16;           // 4 or 3
   static constexpr int A_BYTES = BM * BK * 2;
   static constexpr int B_BYTES = BN * BK * 2;
@@ -165,10 +165,10 @@ template <typename OutT> struct Out {
 // columns.  LDS rows are BN elements; the 16-byte chunks of row R are
 // XOR-permuted by (R / 4) % 4 times 32 bytes, so the four row groups one
 // write instruction touches fall in different banks.  fp32 tiles go through
-// LDS in two passes of 128 rows.  Requires (checked by the launcher) output
+// LDS in two passes of BM / 2 rows.  Requires (checked by the launcher) output
 // row pitches and the column split a multiple of 16 bytes and N of the
 // chunk width.
-template <typename OutT, int BN, bool BIAS>
+template <typename OutT, int BN, int BM, bool BIAS>
 __device__ __forceinline__ void store_tile_staged(const f32x4_t (&acc)[BM / 2 / 16][BN / 4 / 16],
                                                   const Out<OutT>& C, const bf16_t* bias,
                                                   bf16_t* smem, int M, int N, int m0, int n0,
@@ -245,11 +245,11 @@ __device__ __forceinline__ void store_tile_staged(const f32x4_t (&acc)[BM / 2 / 
 
 // ROWSUM: A is m-major; the workgroups of the first column of tiles write
 // the row sums of A over their split's k-range to rowsum[z * M + m].
-template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN>
+template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN, int BM>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
     Op A, Op B, Out<OutT> C, const bf16_t* __restrict__ bias, float* __restrict__ rowsum,
     int M, int N, int K, int kps, int tm, int tn, int S, int staged) {
-  using CF = Cfg<BN>;
+  using CF = Cfg<BN, BM>;
   extern __shared__ __align__(16) bf16_t smem[];
 
   // XCD-contiguous tile order: workgroup b runs on XCD b % 8.
@@ -333,7 +333,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
   }
 
   if (staged) {
-    store_tile_staged<OutT, BN, BIAS>(acc, C, bias, smem, M, N, m0, n0, z, wm, wn, wave, lane);
+    store_tile_staged<OutT, BN, BM, BIAS>(acc, C, bias, smem, M, N, m0, n0, z, wm, wn, wave, lane);
     return;
   }
 #pragma unroll
@@ -355,14 +355,14 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
   }
 }
 
-template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN>
+template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN, int BM = BM0>
 hipError_t launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kps, hipStream_t s) {
-  auto kern = gemm_bf16_kernel<AK, BKM, OutT, BIAS, ROWSUM, BN>;
+  auto kern = gemm_bf16_kernel<AK, BKM, OutT, BIAS, ROWSUM, BN, BM>;
   static bool attr = false;  // per instantiation
   if (!attr) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             Cfg<BN>::LDS);
+                                             Cfg<BN, BM>::LDS);
     if (e != hipSuccess) return e;
     attr = true;
   }
@@ -381,7 +381,8 @@ hipError_t launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kp
   const bool staged = (al & 15) == 0 && g.N % EPC == 0 && dst.ld0 % EPC == 0 &&
                       dst.ld1 % EPC == 0 && (dst.split >= g.N || dst.split % EPC == 0) &&
                       dst.zstride % EPC == 0 && (sizeof(OutT) == 2 || S == 1);
-  hipLaunchKernelGGL(kern, dim3(tm * tn * S), dim3(NT), Cfg<BN>::LDS, s, A, B, dst,
+  constexpr int lds = Cfg<BN, BM>::LDS;
+  hipLaunchKernelGGL(kern, dim3(tm * tn * S), dim3(NT), lds, s, A, B, dst,
                      static_cast<const bf16_t*>(g.bias), rowsum, g.M, g.N, g.K, kps, tm, tn, S,
                      staged ? 1 : 0);
   return hipGetLastError();
@@ -419,7 +420,7 @@ double grid_time(int64_t w, double work) {
 
 // Tile width: 256, or 192 when its grid keeps the CUs busier.
 int pick_bn(int M, int N) {
-  const int64_t tm = (M + BM - 1) / BM;
+  const int64_t tm = (M + BM0 - 1) / BM0;
   const double t256 = grid_time(tm * ((N + 255) / 256), 256.0);
   const double t192 = grid_time(tm * ((N + 191) / 192), 192.0);
   return t192 < t256 ? 192 : 256;
@@ -430,6 +431,23 @@ hipError_t launch_bn(int bn, const GemmArgs& g, Out<OutT> dst, float* rowsum, in
                      hipStream_t s) {
   return bn == 192 ? launch<AK, BKM, OutT, BIAS, ROWSUM, 192>(g, dst, rowsum, S, kps, s)
                    : launch<AK, BKM, OutT, BIAS, ROWSUM, 256>(g, dst, rowsum, S, kps, s);
+}
+
+// Weight gradients in S k-splits (fp32 partials and a reduction when S > 1).
+template <int BN, int BM>
+hipError_t weight_grads(const GemmArgs& g, int S, int ktiles, hipStream_t s) {
+  if (S == 1) {
+    return g.rowsum ? launch<false, false, float, false, true, BN, BM>(g, direct_out<float>(g), g.rowsum, 1, g.K, s)
+                    : launch<false, false, float, false, false, BN, BM>(g, direct_out<float>(g), nullptr, 1, g.K, s);
+  }
+  const int kps = ((ktiles + S - 1) / S) * BK;
+  float* part = g.ws;
+  float* rs_part = g.ws + (int64_t)S * g.M * g.N;
+  Out<float> d{part, g.N, part, g.N, 1 << 30, (int64_t)g.M * g.N};  // one slice per split
+  const hipError_t e = g.rowsum ? launch<false, false, float, false, true, BN, BM>(g, d, rs_part, S, kps, s)
+                                : launch<false, false, float, false, false, BN, BM>(g, d, nullptr, S, kps, s);
+  if (e != hipSuccess) return e;
+  return splitk_reduce_launch(part, S, g, rs_part, s);
 }
 
 }  // namespace
@@ -452,35 +470,29 @@ hipError_t gemm_bf16(const GemmArgs& g, hipStream_t s) {
   if (!g.a_kmajor && !g.b_kmajor && !g.bias && g.c_f32) {  // weight gradients
     // (the row-sum variant keeps within the register budget at BN = 192)
     constexpr int bn = 192;
-    const int64_t tiles = (int64_t)((g.N + bn - 1) / bn) * ((g.M + BM - 1) / BM);
     const int ktiles = (g.K + BK - 1) / BK;
-    // splits: least estimated time = rounds of one workgroup per CU over
-    // the k-range (tiles at ~60 % of the MFMA peak per CU) plus writing and
-    // re-reading the fp32 partials (~4 TB/s)
-    int S = 1;
+    // tile height (256 or 192) and splits: least estimated time = rounds of
+    // one workgroup per CU over the k-range (tiles at ~60 % of the MFMA peak
+    // per CU) plus writing and re-reading the fp32 partials (~4 TB/s).  The
+    // lower tiles fill the 256 CUs where 256-row tiles would leave some idle
+    // (e.g. 12 x 8 tiles of 256 x 192 in 2 splits: 192 workgroups; 16 x 8 of
+    // 192 x 192: 256).
+    int S = 1, bm = BM0;
     if (g.ws) {
-      const double t_tile = 2.0 * BM * bn * (double)g.K / (2.5e15 / device_cus() * 0.6);
       const double t_part = (double)g.M * g.N * 8.0 / 4e12;
       double best = 1e30;
-      for (int c = 1; c <= 8; ++c) {
-        if (c > 1 && ktiles / c < 8) break;  // at least 8 k-tiles per split
-        if (c > 1 && (int64_t)c * g.M * g.N + (int64_t)c * g.M > g.ws_floats) break;
-        const double cost = grid_time(tiles * c, t_tile / c) + (c > 1 ? c * t_part : 0.0);
-        if (cost < best) { best = cost; S = c; }
+      for (int h : {BM0, 192}) {
+        const int64_t tiles = (int64_t)((g.N + bn - 1) / bn) * ((g.M + h - 1) / h);
+        const double t_tile = 2.0 * h * bn * (double)g.K / (2.5e15 / device_cus() * 0.6);
+        for (int c = 1; c <= 8; ++c) {
+          if (c > 1 && ktiles / c < 8) break;  // at least 8 k-tiles per split
+          if (c > 1 && (int64_t)c * g.M * g.N + (int64_t)c * g.M > g.ws_floats) break;
+          const double cost = grid_time(tiles * c, t_tile / c) + (c > 1 ? c * t_part : 0.0);
+          if (cost < best - 1e-12) { best = cost; S = c; bm = h; }
+        }
       }
     }
-    if (S == 1) {
-      return g.rowsum ? launch<false, false, float, false, true, bn>(g, direct_out<float>(g), g.rowsum, 1, g.K, s)
-                      : launch<false, false, float, false, false, bn>(g, direct_out<float>(g), nullptr, 1, g.K, s);
-    }
-    const int kps = ((ktiles + S - 1) / S) * BK;
-    float* part = g.ws;
-    float* rs_part = g.ws + (int64_t)S * g.M * g.N;
-    Out<float> d{part, g.N, part, g.N, 1 << 30, (int64_t)g.M * g.N};  // one slice per split
-    const hipError_t e = g.rowsum ? launch<false, false, float, false, true, bn>(g, d, rs_part, S, kps, s)
-                                  : launch<false, false, float, false, false, bn>(g, d, nullptr, S, kps, s);
-    if (e != hipSuccess) return e;
-    return splitk_reduce_launch(part, S, g, rs_part, s);
+    return bm == 192 ? weight_grads<bn, 192>(g, S, ktiles, s) : weight_grads<bn, BM0>(g, S, ktiles, s);
   }
   return hipErrorInvalidValue;
 }
