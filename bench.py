@@ -112,6 +112,27 @@ def step_flops(w, T, lengths):
     return per_frame * N, N
 
 
+_CYCLES_PER_MS = None
+
+
+def _hold_gpu(ms):
+    """Keep the GPU busy for about `ms` (torch's spin kernel), so that the
+    launches enqueued next wait in the queue and then run back to back: the
+    events around each launch then time the GPU, not the host's launch path
+    (which is longer than a small kernel)."""
+    import torch
+    global _CYCLES_PER_MS
+    if _CYCLES_PER_MS is None:
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(1000)
+        a.record()
+        torch.cuda._sleep(1_000_000)
+        b.record()
+        b.synchronize()
+        _CYCLES_PER_MS = 1_000_000 / max(a.elapsed_time(b), 1e-3)
+    torch.cuda._sleep(int(ms * _CYCLES_PER_MS))
+
+
 def _hbm_entry(kt, reps):
     us = kt["ms"] * 1e3 / max(kt["launches"], 1)
     per_launch = kt["bytes"] / max(kt["launches"], 1)
@@ -142,6 +163,7 @@ def worker_kernels(am, n, reps):
     local = torch.empty(n, device=dev)
     local_bf = torch.empty(n, dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()
+    _hold_gpu(5.0)
     am.profile_begin([am.K_BMUF])
     for _ in range(reps):
         am.bmuf_block_update(models, S, wg, delta, 0.875, 0.875, 1.0, local, local_bf)
@@ -163,6 +185,7 @@ def worker_kernels(am, n, reps):
     dws = torch.zeros(am.decode_multi_workspace_bytes(S, n), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
     total_words = int(counts.sum())
+    _hold_gpu(5.0)
     am.profile_begin([am.K_DECODE])
     for _ in range(reps):
         am.grad_threshold_decode_multi(words, counts, tau, dense, dws)
@@ -193,21 +216,25 @@ def hbm_kernels(am, synth, w, n, reps):
     gen.manual_seed(8)
     flush = torch.zeros(1 << 28, device=dev)  # 1 GiB
 
-    def timed(cls, launch, extra_bytes=lambda: 0.0):
+    def timed(cls, launch, count=None):
+        # count: device word count of each launch (4 bytes per word are
+        # added to the library's per-element bytes), summed on the device
         res = {}
         for mode in ("in_loop", "flushed"):
             launch()
             torch.cuda.synchronize()
-            extra = 0.0
+            words = torch.zeros(1, dtype=torch.int64, device=dev)
+            _hold_gpu(5.0)
             am.profile_begin([cls])
             for i in range(reps):
                 if mode == "flushed":
                     flush.sum()
                 launch()
-                extra += extra_bytes()
+                if count is not None:
+                    words += count
             am.profile_end()
             kt = am.profile_get(cls)
-            res[mode] = _hbm_entry(dict(kt, bytes=kt["bytes"] + extra), reps)
+            res[mode] = _hbm_entry(dict(kt, bytes=kt["bytes"] + 4.0 * float(words.item())), reps)
         return res
 
     out = {}
@@ -228,12 +255,11 @@ def hbm_kernels(am, synth, w, n, reps):
     words = torch.zeros(n, dtype=torch.int32, device=dev)
     count = torch.zeros(1, dtype=torch.int64, device=dev)
     ews = torch.zeros(am.encode_workspace_bytes(n), dtype=torch.uint8, device=dev)
-    word_bytes = lambda: 4.0 * float(count.item())  # read after each launch's count
     out["encode"] = dict(timed(am.K_ENCODE, lambda: am.grad_threshold_encode(g, r, tau, words, count, ews),
-                               word_bytes), elements=n, words_last=int(count.item()))
+                               count), elements=n, words_last=int(count.item()))
     dense = torch.empty(n, device=dev)
     out["decode"] = dict(timed(am.K_DECODE, lambda: am.grad_threshold_decode(words, count, tau, dense),
-                               word_bytes), elements=n, words=int(count.item()))
+                               count), elements=n, words=int(count.item()))
     master = torch.randn(n, generator=gen, device=dev) * 0.03
     wbf = torch.empty(n, dtype=torch.bfloat16, device=dev)
     out["sgd"] = dict(timed(am.K_SGD, lambda: am.sgd_apply(master, g, 1e-6, wbf)), elements=n)
@@ -260,12 +286,14 @@ def input_kernels(am, synth, w, N, reps):
     mo = torch.empty((T * B,), dtype=torch.uint8, device="cuda")
     torch.cuda.synchronize()
     out = {}
+    _hold_gpu(5.0)
     am.profile_begin([am.K_MISC])
     for _ in range(reps):
         am.lfr_features(U, raw, mean, std, x)
     am.profile_end()
     out["lfr_features"] = dict(_hbm_entry(am.profile_get(am.K_MISC), reps), frames=T * B,
                                raw_frames=int(U.sum()))
+    _hold_gpu(5.0)
     am.profile_begin([am.K_MISC])
     for _ in range(reps):
         am.delay_targets(T, B, idx, prob, io, po, mo, 3)
@@ -295,20 +323,25 @@ def teacher_kernels(am, synth, w, reps):
     prob = torch.empty_like(val)
     am.blstm_teacher_forward(m, params, x, T, B, logits, ws)  # warm-up
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    _hold_gpu(5.0)
+    e0.record()
     for _ in range(reps):
         am.blstm_teacher_forward(m, params, x, T, B, logits, ws)
-    torch.cuda.synchronize()
-    dt = (time.perf_counter() - t0) / reps
+    e1.record()
+    e1.synchronize()
+    dt = e0.elapsed_time(e1) * 1e-3 / reps
     am.workspace_check(ws)
     out = {"teacher_forward": {"ms_per_batch": round(dt * 1e3, 3),
                                "frames_per_s": round(T * B / dt, 1),
                                "params": n, "frames": T * B}}
+    _hold_gpu(5.0)
     am.profile_begin([am.K_MISC])
     for _ in range(reps):
         am.kbest_logits(logits, idx, val)
     am.profile_end()
     out["kbest_logits"] = dict(_hbm_entry(am.profile_get(am.K_MISC), reps), k=K)
+    _hold_gpu(5.0)
     am.profile_begin([am.K_MISC])
     for _ in range(reps):
         am.kbest_posteriors(val, prob)

@@ -10,8 +10,8 @@
 // stacked dimension walking the frames in order with the running sum in
 // fp64; each value is evaluated in fp64 in the order of the definition with
 // no fused multiply-add and rounded once to the output type, so the output is
-// bit-identical to the element-wise definition.  Loads of the next frames
-// are issued ahead of the running sum.
+// bit-identical to the element-wise definition.  Loads of the next 32 frames
+// are kept in flight ahead of the running sum.
 //
 // delay_targets: the targets of the packed rows shifted by `delay` frames
 // within each sequence (the model's look-ahead): row (t, b) takes the target
@@ -63,7 +63,8 @@ __global__ __launch_bounds__(256) void lfr_features_kernel(LfrArgs a) {
     double run = 0.0;
     int64_t off = 0;  // packed offset of frame t
     int nb = a.B;     // sequences longer than t
-    constexpr int AH = 8;  // frames whose loads are in flight
+    constexpr int AH = 32;  // frames whose loads are in flight (one utterance per
+                            // workgroup: fewer would leave HBM latency exposed)
     float ahead[AH];
 #pragma unroll
     for (int q = 0; q < AH; ++q)
