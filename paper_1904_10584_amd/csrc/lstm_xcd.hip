@@ -9,9 +9,9 @@
 // the exchange and the step barrier stay inside one L2:
 //   * with m workgroups per block, workgroup i serves block i % 8 + 8 (i / 8m)
 //     and unit slice (i / 8) % m (workgroups are dispatched to XCDs
-//     round-robin); at start every workgroup records its
-//     XCC id and, unless every block really is on one XCD, the kernel falls
-//     back to device-scope release/acquire for its whole run;
+//     round-robin); at start every workgroup records its XCC id and, unless
+//     every block really is on one XCD, the kernel falls back to
+//     device-scope release/acquire for its whole run;
 //   * the step barrier is one 128-byte flag line per block: every member
 //     stores its count of completed steps in its own word once its stores
 //     of the step have completed, and one wave polls the line with
@@ -23,8 +23,8 @@
 // W_h resident in registers in unit-major, gate-minor order, so a 16-column
 // MFMA tile holds 4 units x 4 gates; reading the partial tiles back from
 // LDS in 4x4-quad-transposed order then gives each lane all four gate
-// pre-activations of one (sequence, unit).  The backward product keeps the U columns of W_h in
-// registers too.
+// pre-activations of one (sequence, unit).  The backward product keeps the
+// U columns of W_h in registers too.
 #include <cstdlib>
 
 #include "am_device.h"
