@@ -11,8 +11,11 @@
 //
 // topk_rows: the k largest logits of each row in descending order (equal
 // values by ascending index, NaN after every number), one wave per row with
-// the row held in registers as order-preserving integer keys; k rounds of a
-// wave-wide arg-max over the entries not yet taken.
+// the row held in registers as order-preserving integer keys.  Each lane
+// finds its best two entries in one pass; each of the k rounds takes the
+// wave-wide best of the lanes' current entries, and the lane that held it
+// moves to its next: the second from the pass, then each time a scan for
+// its best entry below the one taken.
 //
 // kbest_posterior_rows: the posterior rebuilt from k stored logits with the
 // missing ones at -infinity, i.e. the softmax over the k values (fp32).
@@ -72,48 +75,84 @@ __device__ __forceinline__ uint32_t logit_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-template <int CPL>
+template <int CPL, bool VEC>
 __global__ __launch_bounds__(256) void topk_rows_kernel(int64_t N, int C, int K,
                                                         const float* __restrict__ z,
                                                         int32_t* __restrict__ idx,
                                                         float* __restrict__ val) {
+  static_assert(CPL % 4 == 0, "registers in fours");
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= N) return;
   const float* zr = z + row * C;
+  // register q holds class cls(q): with VEC (C % 4 == 0) four consecutive
+  // classes per 16-byte load, else one class per 64-lane stride
+  auto cls = [&](int q) {
+    return VEC ? 4 * lane + 256 * (q >> 2) + (q & 3) : lane + 64 * q;
+  };
   uint32_t key[CPL];
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) {
-    const int c = lane + 64 * q;
-    key[q] = c < C ? logit_key(zr[c]) : 0u;
-  }
-  for (int j = 0; j < K; ++j) {
-    // this lane's best: the largest key, the first (lowest index) on ties
-    uint32_t bk = 0u;
-    int bq = 0;
+  for (int q4 = 0; q4 < CPL / 4; ++q4) {
+    if (VEC) {
+      const int c = 4 * lane + 256 * q4;
+      const float4 f = c < C ? *reinterpret_cast<const float4*>(zr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      key[4 * q4 + 0] = c < C ? logit_key(f.x) : 0u;
+      key[4 * q4 + 1] = c < C ? logit_key(f.y) : 0u;
+      key[4 * q4 + 2] = c < C ? logit_key(f.z) : 0u;
+      key[4 * q4 + 3] = c < C ? logit_key(f.w) : 0u;
+    } else {
 #pragma unroll
-    for (int q = 0; q < CPL; ++q) {
-      const bool better = key[q] > bk;
-      bk = better ? key[q] : bk;
-      bq = better ? q : bq;
+      for (int e = 0; e < 4; ++e) {
+        const int c = cls(4 * q4 + e);
+        key[4 * q4 + e] = c < C ? logit_key(zr[c]) : 0u;
+      }
     }
-    uint64_t cand = bk ? ((uint64_t)bk << 32) | (uint32_t)~(uint32_t)(lane + 64 * bq) : 0ull;
+  }
+  // candidate of register q: (key << 32) | ~class, unique per class, larger
+  // = earlier in the output; 0 for no class
+  auto cand = [&](int q) -> uint64_t {
+    return key[q] ? ((uint64_t)key[q] << 32) | (uint32_t)~(uint32_t)cls(q) : 0ull;
+  };
+  // this lane's best two candidates, from one pass over its registers
+  uint64_t b0 = 0ull, b1 = 0ull;
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
+    const uint64_t v = cand(q);
+    const bool g0 = v > b0, g1 = v > b1;
+    b1 = g0 ? b0 : (g1 ? v : b1);
+    b0 = g0 ? v : b0;
+  }
+  bool second = true;  // b1 still holds this lane's next candidate
+  int mine = -1;       // lane j keeps the class of round j
+  for (int j = 0; j < K; ++j) {
+    uint64_t best = b0;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
-      const uint64_t other = __shfl_xor(cand, o, 64);
-      cand = other > cand ? other : cand;
+      const uint64_t other = __shfl_xor(best, o, 64);
+      best = other > best ? other : best;
     }
-    if (cand == 0ull) {  // fewer than K entries
-      if (lane == 0) { idx[row * K + j] = -1; val[row * K + j] = -INFINITY; }
-      continue;
-    }
-    const int c = (int)~(uint32_t)cand;
-    if ((c & 63) == lane) {
+    if (best == 0ull) continue;  // fewer than K entries: -1 below
+    if (lane == j) mine = (int)~(uint32_t)best;
+    if (b0 == best) {  // the lane that held it takes its next candidate
+      if (second) {
+        b0 = b1;
+        second = false;
+      } else {  // the best of its candidates below the one taken
+        uint64_t m = 0ull;
 #pragma unroll
-      for (int q = 0; q < CPL; ++q)
-        if (q == (c >> 6)) key[q] = 0u;
+        for (int q = 0; q < CPL; ++q) {
+          const uint64_t v = cand(q);
+          m = (v < best && v > m) ? v : m;
+        }
+        b0 = m;
+      }
     }
-    if (lane == 0) { idx[row * K + j] = c; val[row * K + j] = zr[c]; }
+  }
+  // the k results, one lane each (values reloaded from the row: exact,
+  // signed zeros and NaN payloads included)
+  if (lane < K) {
+    idx[row * K + lane] = mine;
+    val[row * K + lane] = mine >= 0 ? zr[mine] : -INFINITY;
   }
 }
 
@@ -153,8 +192,12 @@ hipError_t gather_rows(const GatherRows& a, bool bf16, hipStream_t s) {
 
 #define AM_TOPK_CASE(CPL_)                                                                    \
   if (cpl <= CPL_) {                                                                          \
-    hipLaunchKernelGGL(topk_rows_kernel<CPL_>, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, s, \
-                       N, C, K, z, idx, val);                                                 \
+    if (vec)                                                                                  \
+      hipLaunchKernelGGL((topk_rows_kernel<CPL_, true>), dim3((unsigned)((N + 3) / 4)),        \
+                         dim3(256), 0, s, N, C, K, z, idx, val);                               \
+    else                                                                                      \
+      hipLaunchKernelGGL((topk_rows_kernel<CPL_, false>), dim3((unsigned)((N + 3) / 4)),       \
+                         dim3(256), 0, s, N, C, K, z, idx, val);                               \
     return hipGetLastError();                                                                 \
   }
 
@@ -162,6 +205,8 @@ hipError_t topk_rows(int64_t N, int C, int K, const float* z, int32_t* idx, floa
                      hipStream_t s) {
   if (N == 0 || K == 0) return hipSuccess;
   const int cpl = (C + 63) / 64;
+  // 16-byte row loads need every row start 16-byte aligned
+  const bool vec = C % 4 == 0 && (reinterpret_cast<uintptr_t>(z) & 15) == 0;
   AM_TOPK_CASE(16) AM_TOPK_CASE(32) AM_TOPK_CASE(48) AM_TOPK_CASE(64) AM_TOPK_CASE(96)
   AM_TOPK_CASE(128)
   return hipErrorInvalidValue;

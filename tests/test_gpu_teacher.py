@@ -74,7 +74,9 @@ def test_teacher_paper_scale_sampled_sequences():
         assert err <= 2e-2
 
 
-@pytest.mark.parametrize("C,K", [(520, 1), (520, 20), (3000, 20), (6000, 64), (64, 64)])
+# (C % 4 != 0 takes the kernel's 4-byte-load path, the others its 16-byte one)
+@pytest.mark.parametrize("C,K", [(520, 1), (520, 20), (3000, 20), (6000, 64), (64, 64),
+                                 (517, 20), (3001, 33)])
 def test_kbest_logits_bit_exact(C, K):
     rng = np.random.default_rng(C + K)
     N = 1037
