@@ -94,6 +94,42 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ sr
   }
 }
 
+// bf16 with both dimensions multiples of 8 and 16-byte aligned rows: 64 x 64
+// tiles moved as 16-byte chunks (eight elements) on both sides, transposed
+// through LDS.  Thread (column, row chunk) gathers eight rows of one column.
+// The chunks of tile row i sit XOR-permuted by (i / 8) % 8, so the eight
+// rows 8 apart that the lanes of one read touch fall in different banks.
+__global__ __launch_bounds__(256) void transpose_bf16_x8(const bf16_t* __restrict__ src,
+                                                         bf16_t* __restrict__ dst, int rows,
+                                                         int cols) {
+  __shared__ __align__(16) bf16_t tile[64 * 64];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  auto at = [](int i, int j) { return i * 64 + (((j >> 3) ^ ((i >> 3) & 7)) << 3) + (j & 7); };
+  // 64 rows x 8 chunks: thread t loads chunks t and t + 256
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int e = threadIdx.x + 256 * h, i = e >> 3, ch = e & 7;
+    const int r = r0 + i, c = c0 + ch * 8;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (r < rows && c < cols) v = *reinterpret_cast<const uint4*>(src + (int64_t)r * cols + c);
+    *reinterpret_cast<uint4*>(&tile[at(i, ch * 8)]) = v;
+  }
+  __syncthreads();
+  // 64 columns x 8 row chunks: thread t writes chunks t and t + 256
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int e = threadIdx.x + 256 * h, j = e >> 3, rc = e & 7;
+    const int c = c0 + j, r = r0 + rc * 8;
+    if (c < cols && r < rows) {
+      uint32_t w[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        w[k] = (uint32_t)tile[at(rc * 8 + 2 * k, j)] | ((uint32_t)tile[at(rc * 8 + 2 * k + 1, j)] << 16);
+      *reinterpret_cast<uint4*>(dst + (int64_t)c * rows + r) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+}
+
 // Partial column sums over a chunk of rows; partial[chunk][c].
 template <typename T>
 __global__ __launch_bounds__(256) void colsum_partial(const T* __restrict__ in, int64_t rows,
@@ -187,7 +223,10 @@ hipError_t fill_zero(float* dst, int64_t n, hipStream_t s) {
 
 hipError_t transpose(const void* src, void* dst, int rows, int cols, bool bf16, hipStream_t s) {
   dim3 grid((cols + 63) / 64, (rows + 63) / 64);
-  if (bf16) hipLaunchKernelGGL(transpose_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)src, (bf16_t*)dst, rows, cols);
+  const bool x8 = rows % 8 == 0 && cols % 8 == 0 &&
+                  ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15) == 0;
+  if (bf16 && x8) hipLaunchKernelGGL(transpose_bf16_x8, grid, dim3(256), 0, s, (const bf16_t*)src, (bf16_t*)dst, rows, cols);
+  else if (bf16) hipLaunchKernelGGL(transpose_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)src, (bf16_t*)dst, rows, cols);
   else hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(256), 0, s, (const float*)src, (float*)dst, rows, cols);
   return hipGetLastError();
 }
