@@ -185,26 +185,29 @@ bool device_persistent_enabled() {
   return persistent_enabled() && !(r && strcmp(r, "xcd") == 0);
 }
 
-// Scratch of the persistent kernels: the sync region at offset 0 of the
-// workspace.  Its first SYNC_CLEAR_WORDS words (step counters, start counter,
-// XCC ids) are zeroed before every launch; its last word is the barrier
-// time-out flag, zeroed once per forward pass and only ever set afterwards,
+// Scratch of the persistent kernels: the sync area at offset 0 of the
+// workspace, one SYNC_BYTES slot per recurrence launch of a pass (each
+// launch's step flags, start counter and XCC ids), so that one clear at the
+// start of a pass serves all its launches instead of one small clear kernel
+// before each.  The last word of slot 0 is the barrier time-out flag of
+// every launch, zeroed once per forward pass and only ever set afterwards,
 // so a time-out anywhere in a forward + backward pair stays visible to
 // am_workspace_check.
 constexpr int64_t SYNC_BYTES = 8192;
-constexpr int64_t SYNC_CLEAR_WORDS = SYNC_BYTES / 4 - 64;
 constexpr int64_t SYNC_STICKY_WORD = SYNC_BYTES / 4 - 1;
-am::XcdSync xcd_sync(void* base) {
-  unsigned* u = static_cast<unsigned*>(base);
+void* sync_slot(void* area, int k) { return static_cast<char*>(area) + (int64_t)k * SYNC_BYTES; }
+int* sync_err(void* area) { return static_cast<int*>(area) + SYNC_STICKY_WORD; }
+am::XcdSync xcd_sync(void* slot, int* err) {
+  unsigned* u = static_cast<unsigned*>(slot);
   am::XcdSync y;
   y.flags = u;             // flag line of block k < 16: u[32 k .. 32 k + 31], a word per member
   y.start = u + 512;
-  y.err = reinterpret_cast<int*>(u + SYNC_STICKY_WORD);
+  y.err = err;
   y.xcc = reinterpret_cast<int*>(u + 516);  // up to 1024 workgroups
   y.units = 0;
   return y;
 }
-static_assert(516 + 1024 <= SYNC_CLEAR_WORDS, "sync region: counters, start word and XCC ids are cleared");
+static_assert(516 + 1024 < SYNC_STICKY_WORD, "a slot holds the flag lines, start word and XCC ids below the time-out word");
 
 am::PersistSchedule persist_schedule(const Schedule& sc) {
   am::PersistSchedule ps;
@@ -234,8 +237,9 @@ WsLayout ws_layout(const am_model* m, int64_t B, int64_t N) {
   const int64_t e = esz_of(m->dtype), H = m->hidden, G = 4 * H, L = m->layers;
   int64_t pos = 0;
   auto take = [&](int64_t bytes) { int64_t at = pos; pos += align256(bytes); return at; };
-  // step-barrier scratch of the persistent kernels and the time-out flag
-  w.sync = take(SYNC_BYTES);
+  // step-barrier scratch of the persistent kernels (a slot per layer and
+  // direction of the pass) and the time-out flag
+  w.sync = take(2 * L * SYNC_BYTES);
   for (int l = 0; l < L; ++l) {
     w.h.push_back(take(N * H * e));
     w.hs.push_back(take(N * H * e));
@@ -268,7 +272,8 @@ struct FwdLayer {
   const void* h0;     // [B][H] activation type, or null (zero)
   const float* c0;    // [B][H]
   void* H; void* Hs; float* C; void* G;  // outputs [N][H], [N][H], [N][H], [N][4H]
-  void* sync;         // the workspace's sync region
+  void* sync;         // this launch's slot of the workspace's sync area (cleared)
+  int* err;           // the time-out flag
 };
 
 am_status forward_recurrence(const FwdLayer& f, const Schedule& sc, bool bf, int64_t H,
@@ -286,21 +291,19 @@ am_status forward_recurrence(const FwdLayer& f, const Schedule& sc, bool bf, int
     pa.C = f.C;
     pa.G = f.G;
     pa.counters = static_cast<unsigned*>(f.sync);
-    pa.err = static_cast<int*>(f.sync) + SYNC_STICKY_WORD;
+    pa.err = f.err;
     pa.hidden = (int)H;
     const am::PersistSchedule ps = persist_schedule(sc);
     const double flops = 2.0 * sc.N * G * H;
     const double bytes = (double)sc.N * (G * e * 2 + H * (2 * e + 4)) + (double)G * H * e;
     bool used = false;
     if (bf && xcd_enabled() && am::lstm_xcd_instantiated(true, (int)H, B)) {
-      AM_TRY(hip_check(am::fill_zero(static_cast<float*>(f.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
       Timed tm(AM_K_LSTM_FWD, s, flops, bytes);
-      AM_TRY(hip_check(am::lstm_fwd_xcd_launch(pa, ps, xcd_sync(f.sync), s, &used),
+      AM_TRY(hip_check(am::lstm_fwd_xcd_launch(pa, ps, xcd_sync(f.sync, f.err), s, &used),
                        "lstm forward layer (xcd)"));
       if (!used) tm.cancel();
     }
     if (!used && device_persistent_enabled() && am::lstm_persistent_fits(true, (int)H, B, bf, T)) {
-      AM_TRY(hip_check(am::fill_zero(static_cast<float*>(f.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
       Timed tm(AM_K_LSTM_FWD, s, flops, bytes);
       AM_TRY(hip_check(am::lstm_fwd_persistent(pa, ps, bf, s, &used), "lstm forward layer"));
       if (!used) tm.cancel();
@@ -418,7 +421,7 @@ TeacherWs teacher_ws_layout(const am_model* m, int64_t T, int64_t B, int64_t N) 
   const int64_t Dmax = m->input_dim > 2 * H ? m->input_dim : 2 * H;
   int64_t pos = 0;
   auto take = [&](int64_t bytes) { int64_t at = pos; pos += align256(bytes); return at; };
-  w.sync = take(SYNC_BYTES);
+  w.sync = take(2 * m->layers * SYNC_BYTES);  // a slot per layer and direction
   w.offs = take((T + 1) * 8);
   w.lens = take(B * 4);
   w.cat0 = take(N * 2 * H * e);
@@ -699,7 +702,7 @@ am_status blstm_teacher_forward(const am_model* m, const void* params, const voi
     AM_TRY(hip_check(am::schedule_tables(st, s), "schedule tables"));
   }
   AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.c0), B * H, s), "c0 clear"));
-  AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_BYTES / 4, s), "sync clear"));
+  AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), 2 * L * SYNC_BYTES / 4, s), "sync clear"));
   auto gather = [&](const void* src, int64_t src_ld, void* dst, int64_t dst_ld, int64_t col,
                     int width, bool reverse) {
     am::GatherRows g;
@@ -734,7 +737,8 @@ am_status blstm_teacher_forward(const am_model* m, const void* params, const voi
       f.Hs = at<void>(ws, w.hs);
       f.C = at<float>(ws, w.c);
       f.G = at<void>(ws, w.g);
-      f.sync = at<void>(ws, w.sync);
+      f.sync = sync_slot(at<void>(ws, w.sync), k);
+      f.err = sync_err(at<void>(ws, w.sync));
       AM_TRY(forward_recurrence(f, sc, bf, H, s));
       AM_TRY(gather(at<void>(ws, w.hdir), H, out, 2 * H, d * H, (int)H, d == 1));
     }
@@ -821,8 +825,9 @@ am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
     if (c0) AM_TRY(hip_check(am::convert_rows(c0, c0w, L * B * H, false, s), "c0 copy"));
     else AM_TRY(hip_check(am::fill_zero(c0w, L * B * H, s), "c0 clear"));
     if (h0) AM_TRY(hip_check(am::convert_rows(h0, at<void>(ws, w.h0), L * B * H, bf, s), "h0 convert"));
-    // a new forward + backward pair: clear the barrier time-out flag too
-    AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_BYTES / 4, s), "sync clear"));
+    // a new forward + backward pair: every slot of the sync area and the
+    // barrier time-out flag
+    AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), 2 * L * SYNC_BYTES / 4, s), "sync clear"));
   }
 
   for (int l = 0; l < L; ++l) {
@@ -841,7 +846,8 @@ am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
     f.Hs = at<void>(ws, w.hs[l]);
     f.C = at<float>(ws, w.c[l]);
     f.G = at<void>(ws, w.g[l]);
-    f.sync = at<void>(ws, w.sync);
+    f.sync = sync_slot(at<void>(ws, w.sync), l);
+    f.err = sync_err(at<void>(ws, w.sync));
     AM_TRY(forward_recurrence(f, sc, bf, H, s));
   }
   AM_TRY(run_gemm(AM_K_GEMM_FWD,
@@ -896,6 +902,9 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
   const Offsets po = param_layout(m);
   const char* P8 = static_cast<const char*>(params);
   float* skws = at<float>(ws, w.splitk);
+  // the backward launches' slots of the sync area (not slot 0's time-out flag)
+  AM_TRY(hip_check(am::fill_zero(static_cast<float*>(sync_slot(at<void>(ws, w.sync), (int)L)),
+                                 L * SYNC_BYTES / 4, s), "sync clear"));
 
   // output layer: dWo = dZ^T H_top and dbo = column sums of dZ (one pass),
   // then dH_top = dZ Wo
@@ -925,8 +934,9 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
       pa.C = Cl;
       pa.c0 = at<float>(ws, w.c0) + (int64_t)l * B * H;
       pa.dA = dA;
-      pa.counters = at<unsigned>(ws, w.sync);
-      pa.err = at<int>(ws, w.sync) + SYNC_STICKY_WORD;
+      void* slot = sync_slot(at<void>(ws, w.sync), L + l);
+      pa.counters = static_cast<unsigned*>(slot);
+      pa.err = sync_err(at<void>(ws, w.sync));
       pa.hidden = (int)H;
       const am::PersistSchedule ps = persist_schedule(sc);
       const double flops = 2.0 * (sc.N - sc.counts[0]) * G * H;
@@ -936,14 +946,12 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
           Timed tm(AM_K_MISC, s, 0.0, 2.0 * G * H * e);
           AM_TRY(hip_check(am::transpose(P8 + po.wh[l] * e, WhT, (int)G, (int)H, bf, s), "Wh transpose"));
         }
-        AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
         Timed tm(AM_K_LSTM_BWD, s, flops, bytes);
-        AM_TRY(hip_check(am::lstm_bwd_xcd_launch(pa, ps, xcd_sync(at<void>(ws, w.sync)), s, &used),
+        AM_TRY(hip_check(am::lstm_bwd_xcd_launch(pa, ps, xcd_sync(slot, pa.err), s, &used),
                          "lstm backward layer (xcd)"));
         if (!used) tm.cancel();
       }
       if (!used && device_persistent_enabled() && am::lstm_persistent_fits(false, (int)H, B, bf, T)) {
-        AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), SYNC_CLEAR_WORDS, s), "sync clear"));
         Timed tm(AM_K_LSTM_BWD, s, flops, bytes);
         AM_TRY(hip_check(am::lstm_bwd_persistent(pa, ps, bf, s, &used), "lstm backward layer"));
         if (!used) tm.cancel();
