@@ -107,9 +107,8 @@ struct PersistBwd {
 // and the XCC id of every workgroup (xcc[grid]), all zero at launch, and the
 // time-out flag (set, never cleared).
 struct XcdSync {
-  unsigned* flags;
-  unsigned* start;
-  int* xcc;
+  unsigned* flags;  // a 32-word line per block of sequences, a word per member
+  int* xcc;         // the same for the members' XCD ids (check of the layout)
   int* err;
   int units;  // filled in by the launcher
 };

@@ -187,7 +187,7 @@ bool device_persistent_enabled() {
 
 // Scratch of the persistent kernels: the sync area at offset 0 of the
 // workspace, one SYNC_BYTES slot per recurrence launch of a pass (each
-// launch's step flags, start counter and XCC ids), so that one clear at the
+// launch's step flags and XCC ids), so that one clear at the
 // start of a pass serves all its launches instead of one small clear kernel
 // before each.  The last word of slot 0 is the barrier time-out flag of
 // every launch, zeroed once per forward pass and only ever set afterwards,
@@ -200,14 +200,13 @@ int* sync_err(void* area) { return static_cast<int*>(area) + SYNC_STICKY_WORD; }
 am::XcdSync xcd_sync(void* slot, int* err) {
   unsigned* u = static_cast<unsigned*>(slot);
   am::XcdSync y;
-  y.flags = u;             // flag line of block k < 16: u[32 k .. 32 k + 31], a word per member
-  y.start = u + 512;
+  y.flags = u;  // flag line of block k < 16: u[32 k .. 32 k + 31], a word per member
+  y.xcc = reinterpret_cast<int*>(u + 512);  // XCC line of block k: u[512 + 32 k ..], the same
   y.err = err;
-  y.xcc = reinterpret_cast<int*>(u + 516);  // up to 1024 workgroups
   y.units = 0;
   return y;
 }
-static_assert(516 + 1024 < SYNC_STICKY_WORD, "a slot holds the flag lines, start word and XCC ids below the time-out word");
+static_assert(512 + 512 <= SYNC_STICKY_WORD, "a slot holds the flag and XCC lines below the time-out word");
 
 am::PersistSchedule persist_schedule(const Schedule& sc) {
   am::PersistSchedule ps;

@@ -42,29 +42,31 @@ __device__ __forceinline__ unsigned xcc_id() {
   return v & 0xfu;
 }
 
-// One-time check that every block's workgroups share one XCD.  Uses
-// device-scope atomics; returns the same answer in every workgroup.
-__device__ bool check_local(const XcdSync& y, int* bad_sh) {
-  const int n = gridDim.x;
-  if (threadIdx.x == 0) {
-    __hip_atomic_store(y.xcc + blockIdx.x, (int)xcc_id(), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_fetch_add(y.start, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    unsigned spins = 0;
-    while (__hip_atomic_load(y.start, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < (unsigned)n) {
+// One-time check that the workgroups of this block share one XCD: each
+// publishes its XCD (+1; the launch's sync slot starts zeroed) in its word
+// of the block's line, and one wave waits for all members and compares.
+// Only the block's members take part, with plain device-scope loads and
+// stores: no read-modify-write, no cache write-back or invalidation.  Every
+// member of a block returns the same answer.
+__device__ bool check_local(const XcdSync& y, int blk, int us, int members, int* bad_sh) {
+  unsigned* line = reinterpret_cast<unsigned*>(y.xcc) + blk * 32;
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    if (lane == 0) __hip_atomic_store(line + us, xcc_id() + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    unsigned v = 0, spins = 0;
+    for (;;) {
+      v = lane < members ? __hip_atomic_load(line + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 1u;
+      if (__all(v != 0)) break;
       if (++spins > SPIN_LIMIT) {
-        __hip_atomic_store(y.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (lane == 0) __hip_atomic_store(y.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;
       }
       __builtin_amdgcn_s_sleep(2);
     }
-    *bad_sh = 0;
+    const unsigned first = __shfl(v, 0, 64);
+    const bool bad = __any(lane < members && v != first);
+    if (lane == 0) *bad_sh = bad ? 1 : 0;
   }
-  __syncthreads();
-  int bad = 0;
-  for (int k = threadIdx.x; k < n; k += blockDim.x)
-    bad |= __hip_atomic_load(y.xcc + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) !=
-           __hip_atomic_load(y.xcc + (k % NX), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (bad) __hip_atomic_store(bad_sh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   __syncthreads();
   return *bad_sh == 0;
 }
@@ -187,7 +189,7 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
     for (int s = 0; s < KH; ++s)
       wf[ts][s] = frag_load<bf16_t>(Wh + (int64_t)row * H + (kh * KH + s) * 32 + (lane >> 4) * 8);
   }
-  const bool local = check_local(y, &bad_sh);
+  const bool local = check_local(y, blk, us, members, &bad_sh);
 
   // The tiles this wave finishes ("own slots" o < FIN): tile index
   // ts = o (k-half 0) or FIN + o (k-half 1).  The lane's cells in tile t:
@@ -366,7 +368,7 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
     for (int s = 0; s < KW; ++s)
       wb[s][n] = frag_load<bf16_t>(WhT + (int64_t)unit * G4 + (wave * KW + s) * 32 + (lane >> 4) * 8);
   }
-  const bool local = check_local(y, &bad_sh);
+  const bool local = check_local(y, blk, us, members, &bad_sh);
 
   // Cell work: items p = (row tile m, unit tile n, quad row r), MT NTU 4 of
   // them; item p covers, per lane, unit 16n + lane%16 and row
