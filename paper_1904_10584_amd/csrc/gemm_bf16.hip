@@ -65,6 +65,14 @@ template <int BN, int BM> struct Cfg {
 };
 
 typedef short v4s_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// (a, b) -> packed bf16 pair, a in the low half (hardware conversion).
+__device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
+  const f32x2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
 typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
 
 // Element offset of chunk c (8 bf16) of row r in a k-major tile.
@@ -182,6 +190,7 @@ __device__ __forceinline__ void store_tile_staged(const f32x4_t (&acc)[BM / 2 / 
   constexpr int PROWS = BM / PASSES;         // rows per pass
   unsigned char* lds = reinterpret_cast<unsigned char*>(smem);
   auto swz = [](int row, int chunk) { return chunk ^ (((row >> 2) & 3) * (32 / 16)); };
+  const uint32_t odd = (lane & 1) ? 0xFFFFFFFFu : 0u;  // lane parity as a mask
   __syncthreads();  // every wave is done with the stage buffers
 #pragma unroll
   for (int p = 0; p < PASSES; ++p) {
@@ -194,19 +203,23 @@ __device__ __forceinline__ void store_tile_staged(const f32x4_t (&acc)[BM / 2 / 
         for (int i = 0; i < MI; ++i) {
           const int rl = wm + i * 16 + mfma_row(lane, 0) - p * PROWS;  // first of 4 rows
           if (ES == 2) {
-            const uint32_t p01 = (uint32_t)f32_to_bf16(acc[i][j][0] + bv) |
-                                 ((uint32_t)f32_to_bf16(acc[i][j][1] + bv) << 16);
-            const uint32_t p23 = (uint32_t)f32_to_bf16(acc[i][j][2] + bv) |
-                                 ((uint32_t)f32_to_bf16(acc[i][j][3] + bv) << 16);
-            const bool odd = lane & 1;
-            const uint32_t give = odd ? p01 : p23;
+            // rows (0, 1) and (2, 3) of column cl, each pair rounded to bf16
+            // by one hardware conversion (round to nearest; an output, not
+            // a quantity compared bit for bit)
+            const uint32_t p01 = pk_bf16(acc[i][j][0] + bv, acc[i][j][1] + bv);
+            const uint32_t p23 = pk_bf16(acc[i][j][2] + bv, acc[i][j][3] + bv);
+            // odd lanes give p01, even lanes p23 (masks, not per-lane
+            // branches)
+            const uint32_t give = (p01 & odd) | (p23 & ~odd);
             // quad_perm [1,0,3,2]: lane l receives lane l ^ 1
             const uint32_t got = (uint32_t)__builtin_amdgcn_mov_dpp((int)give, 0xB1, 0xF, 0xF, false);
             // even lane: rows 0, 1 of columns (cl, cl + 1); odd lane: rows 2, 3
-            // of columns (cl - 1, cl)
-            const uint32_t w0 = odd ? ((got & 0xFFFFu) | (p23 << 16)) : ((p01 & 0xFFFFu) | (got << 16));
-            const uint32_t w1 = odd ? ((got >> 16) | (p23 & 0xFFFF0000u)) : ((p01 >> 16) | (got & 0xFFFF0000u));
-            const int c0 = cl & ~1, r0 = rl + (odd ? 2 : 0);
+            // of columns (cl - 1, cl).  lo / hi: the lower / upper column's pair.
+            const uint32_t lo = (got & odd) | (p01 & ~odd);
+            const uint32_t hi = (p23 & odd) | (got & ~odd);
+            const uint32_t w0 = __builtin_amdgcn_perm(hi, lo, 0x05040100u);  // first rows
+            const uint32_t w1 = __builtin_amdgcn_perm(hi, lo, 0x07060302u);  // second rows
+            const int c0 = cl & ~1, r0 = rl + ((lane & 1) << 1);
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
               const int row = r0 + h;
