@@ -34,10 +34,15 @@ template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return
 // Saved gate activations of a row: unit j's four gates (i, f, g, o) sit
 // together at 4j .. 4j+3, so one cell's gates move as one 8-byte (bf16) or
 // 16-byte (fp32) access.
+__device__ __forceinline__ uint2 pack_gates(float i, float f, float g, float o) {
+  return make_uint2((uint32_t)f32_to_bf16(i) | ((uint32_t)f32_to_bf16(f) << 16),
+                    (uint32_t)f32_to_bf16(g) | ((uint32_t)f32_to_bf16(o) << 16));
+}
+__device__ __forceinline__ void store_gates(bf16_t* grow, int j, uint2 packed) {
+  *reinterpret_cast<uint2*>(grow + 4 * j) = packed;
+}
 __device__ __forceinline__ void store_gates(bf16_t* grow, int j, float i, float f, float g, float o) {
-  *reinterpret_cast<uint2*>(grow + 4 * j) =
-      make_uint2((uint32_t)f32_to_bf16(i) | ((uint32_t)f32_to_bf16(f) << 16),
-                 (uint32_t)f32_to_bf16(g) | ((uint32_t)f32_to_bf16(o) << 16));
+  store_gates(grow, j, pack_gates(i, f, g, o));
 }
 __device__ __forceinline__ void store_gates(float* grow, int j, float i, float f, float g, float o) {
   *reinterpret_cast<float4*>(grow + 4 * j) = make_float4(i, f, g, o);

@@ -210,6 +210,29 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
     h_reg[o] = h0 ? h0[(int64_t)b * H + j] : (bf16_t)0;
   }
 
+  // The polling wave (wave 0) copies no h rows and stores its cells' cell
+  // state, gates and h_{t-1} (read only by the backward pass) one step late,
+  // right after its next poll: a wave's memory counter retires in order, so
+  // stores issued before the poll would hold up the poll's loads.  Its
+  // cells' values wait in dc / dg / dh (row drow, or -1).
+  float dc[FIN];
+  uint2 dg[FIN];
+  bf16_t dh[FIN];
+  int drow = -1;
+  auto post_stores = [&](int row, const float* cv, const uint2* gv, const bf16_t* hv) {
+#pragma unroll
+    for (int o = 0; o < FIN; ++o) {
+      if (!slot_ok(o)) continue;
+      const int j = unit(o);
+      const int64_t ofs = (int64_t)row * H + j;
+      a.C[ofs] = cv[o];
+      Hs[ofs] = hv[o];
+      store_gates(Gb + (int64_t)row * G4, j, gv[o]);
+    }
+  };
+  // every load so far (weights, state) is complete here, so the compiler
+  // keeps no waits for them inside the loop
+  wait_vm<0>();
   int nb = ps.B, off = 0, off_prev = 0;
   for (int t = 0; t < ps.T; ++t) {
     nb = active_down(ps, nb, t);
@@ -232,17 +255,24 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
       xwait(y, local, blk, members, (unsigned)t);
       hsrc = Hb + (int64_t)off_prev * H;
     }
+    if (wave == 0 && drow >= 0) {
+      post_stores(drow, dc, dg, dh);
+      drow = -1;
+    }
     if (hsrc) {
-      // the block's rows of h_{t-1} (inactive rows read an active one) to LDS
+      // the block's rows of h_{t-1} (inactive rows read an active one) to
+      // LDS, by waves 1-7
       constexpr int RG = RB / 8, NQ = (KS / 2) * RG;
-      for (int q = wave; q < NQ; q += 8) {
-        const int line = q / RG, rg = q % RG;
-        const int r = rg * 8 + (lane >> 3);
-        const int chunk = line * 8 + ((lane & 7) ^ (r & 7));
-        dma16(hsrc + (int64_t)min(b0 + r, nb - 1) * H + chunk * 8,
-              __builtin_amdgcn_readfirstlane(lds_address(hl + (line * RB + rg * 8) * 64)));
+      if (wave > 0) {
+        for (int q = wave - 1; q < NQ; q += 7) {
+          const int line = q / RG, rg = q % RG;
+          const int r = rg * 8 + (lane >> 3);
+          const int chunk = line * 8 + ((lane & 7) ^ (r & 7));
+          dma16(hsrc + (int64_t)min(b0 + r, nb - 1) * H + chunk * 8,
+                __builtin_amdgcn_readfirstlane(lds_address(hl + (line * RB + rg * 8) * 64)));
+        }
+        wait_vm<0>();
       }
-      wait_vm<0>();
       __syncthreads();
       // A fragments in batches of up to four, each batch read before its
       // MFMAs (the resident weights leave room for four in registers)
@@ -306,18 +336,24 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
     }
     xsignal(y, local, blk, us, (unsigned)(t + 1));  // h stores complete; its barrier also orders the LDS reuse
     // stores only the backward pass reads
+    uint2 gp[FIN];
 #pragma unroll
-    for (int o = 0; o < FIN; ++o) {
-      if (!row_ok || !slot_ok(o)) continue;
-      const int j = unit(o);
-      const int64_t ofs = (int64_t)(off + b) * H + j;
-      a.C[ofs] = cnew[o];
-      Hs[ofs] = hprev[o];
-      store_gates(Gb + (int64_t)(off + b) * G4, j, gate[o][0], gate[o][1], gate[o][2], gate[o][3]);
+    for (int o = 0; o < FIN; ++o) gp[o] = pack_gates(gate[o][0], gate[o][1], gate[o][2], gate[o][3]);
+    if (wave != 0) {
+      if (row_ok) post_stores(off + b, cnew, gp, hprev);
+    } else if (row_ok) {
+#pragma unroll
+      for (int o = 0; o < FIN; ++o) {
+        dc[o] = cnew[o];
+        dg[o] = gp[o];
+        dh[o] = hprev[o];
+      }
+      drow = off + b;
     }
     off_prev = off;
     off += nb;
   }
+  if (wave == 0 && drow >= 0) post_stores(drow, dc, dg, dh);
 }
 
 // ---------------------------------------------------------------- backward --
