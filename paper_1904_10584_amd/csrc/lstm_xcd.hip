@@ -150,7 +150,7 @@ __device__ __forceinline__ int active_up(const PersistSchedule& ps, int nb, int 
 // ceil(TPW/2) tiles, the k-half-1 wave the rest.  A step is signalled as soon
 // as its h stores (the only exchanged data) are complete; the cell state,
 // gate and h_{t-1} copies are stored after the signal.
-template <int MT, int KS, int TPW>
+template <int MT, int KS, int TPW, bool STG>
 __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSchedule ps, XcdSync y) {
   constexpr int RB = 16 * MT;             // sequences per block
   constexpr int KH = KS / 2;              // k-steps per wave
@@ -160,6 +160,12 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
   extern __shared__ __align__(16) unsigned char lds[];
   bf16_t* hl = reinterpret_cast<bf16_t*>(lds);
   f32x4_t* red = reinterpret_cast<f32x4_t*>(lds + HS_BYTES);  // [8][TPW][64]
+  // STG (U % 8 == 0): the block's cell states, h_{t-1} copies and gates of
+  // the step, staged as rows of the unit slice (strides padded by 16 bytes,
+  // which spreads a write's 16 rows over the LDS banks) and written out by
+  // waves 1-7 after the signal as 16-byte row chunks: about 100 cache lines
+  // per step instead of 16 per store instruction (768).
+  unsigned char* stC = lds + HS_BYTES + 8 * TPW * 64 * 16;
   __shared__ int bad_sh;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -170,6 +176,9 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
   const int blk = xcd_block(members), us = (blockIdx.x / NX) % members;
   const int b0 = blk * RB, j0 = us * U;
   const int mw = g % MT;
+  const int CSB = U * 4 + 16, HSB = U * 2 + 16, GSB = U * 8 + 16;  // staged row strides
+  unsigned char* stH = stC + RB * CSB;
+  unsigned char* stG = stH + RB * HSB;
   const bf16_t* __restrict__ P = static_cast<const bf16_t*>(a.P);
   const bf16_t* __restrict__ Wh = static_cast<const bf16_t*>(a.Wh);
   const bf16_t* __restrict__ h0 = static_cast<const bf16_t*>(a.h0);
@@ -210,11 +219,12 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
     h_reg[o] = h0 ? h0[(int64_t)b * H + j] : (bf16_t)0;
   }
 
-  // The polling wave (wave 0) copies no h rows and stores its cells' cell
-  // state, gates and h_{t-1} (read only by the backward pass) one step late,
-  // right after its next poll: a wave's memory counter retires in order, so
-  // stores issued before the poll would hold up the poll's loads.  Its
-  // cells' values wait in dc / dg / dh (row drow, or -1).
+  // The polling wave (wave 0) copies no h rows and issues no stores between
+  // the signal and its next poll: a wave's memory counter retires in order,
+  // so stores issued before the poll would hold up the poll's loads.  With
+  // STG the staged rows are written out by waves 1-7; without, wave 0 stores
+  // its cells' cell state, gates and h_{t-1} one step late, right after its
+  // next poll, from dc / dg / dh (row drow, or -1).
   float dc[FIN];
   uint2 dg[FIN];
   bf16_t dh[FIN];
@@ -332,10 +342,48 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
         Hb[(int64_t)(off + b) * H + unit(o)] = h;
         c_reg[o] = cnew[o];
         h_reg[o] = h;
+        if constexpr (STG) {
+          const int u = unit(o) - j0;
+          *reinterpret_cast<float*>(stC + qrow * CSB + 4 * u) = cnew[o];
+          *reinterpret_cast<bf16_t*>(stH + qrow * HSB + 2 * u) = hprev[o];
+          *reinterpret_cast<uint2*>(stG + qrow * GSB + 8 * u) =
+              pack_gates(gate[o][0], gate[o][1], gate[o][2], gate[o][3]);
+        }
       }
     }
     xsignal(y, local, blk, us, (unsigned)(t + 1));  // h stores complete; its barrier also orders the LDS reuse
     // stores only the backward pass reads
+    if constexpr (STG) {
+      // 16-byte chunks of the staged rows: C, then Hs, then G; chunk e of a
+      // section with cpr chunks per row is row e / cpr (by a multiply: e is
+      // small), chunk e % cpr
+      if (wave > 0) {
+        const int cC = U / 4, cH = U / 8, cG = U / 2;
+        const int nC = RB * cC, nH = RB * cH, nG = RB * cG;
+        auto divr = [](int e, int d) { return (int)(((unsigned)e * ((65536u + d - 1) / d)) >> 16); };
+        for (int e = threadIdx.x - 64; e < nC + nH + nG; e += 448) {
+          int r, c;
+          const unsigned char* src;
+          void* dst;
+          if (e < nC) {
+            r = divr(e, cC); c = e - r * cC;
+            src = stC + r * CSB + 16 * c;
+            dst = a.C + (int64_t)(off + b0 + r) * H + j0 + 4 * c;
+          } else if (e < nC + nH) {
+            const int f = e - nC;
+            r = divr(f, cH); c = f - r * cH;
+            src = stH + r * HSB + 16 * c;
+            dst = Hs + (int64_t)(off + b0 + r) * H + j0 + 8 * c;
+          } else {
+            const int f = e - nC - nH;
+            r = divr(f, cG); c = f - r * cG;
+            src = stG + r * GSB + 16 * c;
+            dst = Gb + (int64_t)(off + b0 + r) * G4 + 4 * j0 + 8 * c;
+          }
+          if (b0 + r < nb) *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src);
+        }
+      }
+    } else {
     uint2 gp[FIN];
 #pragma unroll
     for (int o = 0; o < FIN; ++o) gp[o] = pack_gates(gate[o][0], gate[o][1], gate[o][2], gate[o][3]);
@@ -349,6 +397,7 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
         dh[o] = hprev[o];
       }
       drow = off + b;
+    }
     }
     off_prev = off;
     off += nb;
@@ -611,9 +660,9 @@ XShape xshape(int H, int B) {
 
 }  // namespace
 
-#define AM_FWD_CASE(MT_, KS_, TPW_)                                                      \
-  if (x.MT == MT_ && x.KS == KS_ && x.TPW == TPW_)                                       \
-    return coop(lstm_fwd_xcd<MT_, KS_, TPW_>, blocks, 512, lds, args, s, used);
+#define AM_FWD_CASE(MT_, KS_, TPW_, STG_)                                                \
+  if (x.MT == MT_ && x.KS == KS_ && x.TPW == TPW_ && (x.U % 8 == 0) == STG_)             \
+    return coop(lstm_fwd_xcd<MT_, KS_, TPW_, STG_>, blocks, 512, lds, args, s, used);
 
 hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used) {
   *used = false;
@@ -621,13 +670,16 @@ hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipS
   if (!x.ok) return hipSuccess;
   y.units = x.U;
   const int blocks = NX * x.BPX * (a.hidden / x.U);
-  const size_t lds = (size_t)16 * x.MT * x.KS * 64 + 8 * x.TPW * 64 * 16;
+  // h rows, partial tiles, and (U % 8 == 0) the staged rows of C, Hs and G
+  const size_t lds = (size_t)16 * x.MT * x.KS * 64 + 8 * x.TPW * 64 * 16 +
+                     (x.U % 8 == 0 ? (size_t)16 * x.MT * (14 * x.U + 48) : 0);
   void* args[] = {&a, &ps, &y};
   // instantiated shapes: H = 768 (B <= 128, B <= 256 in blocks of 16 or 32),
   // H = 64, 128
-  AM_FWD_CASE(1, 24, 3) AM_FWD_CASE(2, 24, 3) AM_FWD_CASE(1, 24, 2)
-  AM_FWD_CASE(2, 2, 1) AM_FWD_CASE(1, 2, 1)
-  AM_FWD_CASE(2, 4, 1) AM_FWD_CASE(1, 4, 1)
+  AM_FWD_CASE(1, 24, 3, true) AM_FWD_CASE(2, 24, 3, true) AM_FWD_CASE(1, 24, 2, true)
+  AM_FWD_CASE(2, 2, 1, false) AM_FWD_CASE(1, 2, 1, false)
+  AM_FWD_CASE(2, 4, 1, false) AM_FWD_CASE(1, 4, 1, false)
+  AM_FWD_CASE(2, 4, 1, true) AM_FWD_CASE(1, 4, 1, true)
   return hipSuccess;
 }
 
