@@ -8,8 +8,10 @@
 //     16 bytes per lane), which moves about 2.5x the bytes per CU per clock
 //     of loads into VGPRs; fed through VGPRs, a GEMM tops out near a
 //     quarter of the MFMA peak;
-//   * one wave per SIMD issues MFMAs at half the rate two waves do, so a
-//     workgroup is eight waves (two per SIMD, one workgroup per CU);
+//   * a workgroup is eight waves (two per SIMD, one workgroup per CU): a
+//     single wave issues independent MFMAs at about 87 % of the peak, but
+//     four waves with 128 x 128 tiles each ran ~35 % slower than eight, not
+//     covering their LDS waits;
 //   * a 256 x BN tile (BN = 256, or 192 where that fills the CUs) with waves
 //     of 128 x BN/4 reads 384 bytes or less of LDS per MFMA.
 // Tiles keep their global layout in LDS:

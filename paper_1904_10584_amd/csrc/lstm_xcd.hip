@@ -137,13 +137,15 @@ __device__ __forceinline__ int active_up(const PersistSchedule& ps, int nb, int 
 }
 
 // ----------------------------------------------------------------- forward --
-// Eight waves, two per SIMD (one wave per SIMD issues MFMAs at half the
-// rate two can).  Tile group g = wave % 4 owns the output tiles t = g + 4 ts
+// Eight waves, two per SIMD (a single wave can issue independent MFMAs at
+// about 87 % of the peak, but not also cover its own LDS and memory waits).
+// Tile group g = wave % 4 owns the output tiles t = g + 4 ts
 // (row tile t % MT, column tile t / MT; all tiles of a group share row tile
 // g % MT); k-half kh = wave / 4 multiplies k-steps [kh KS/2, (kh+1) KS/2).
 // The W_h fragments of a wave's tiles and k-steps stay in its registers for
-// the whole launch.  Each step the block's rows of h_{t-1} are copied to
-// LDS with direct loads (whole 128-byte lines), laid out line-major
+// the whole launch.  Each step wave 0 polls the step barrier and waves 1-7
+// copy the block's rows of h_{t-1} to LDS with direct loads (whole 128-byte
+// lines), laid out line-major
 // [H/64 lines][RB rows][128 B] with the 16-byte chunks of a row XOR-swizzled
 // by row, and read back as MFMA fragments.  The two k-halves of a group
 // publish their partial tiles to LDS: the k-half-0 wave finishes the first
