@@ -459,14 +459,25 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
 
   // Cell work: items p = (row tile m, unit tile n, quad row r), MT NTU 4 of
   // them; item p covers, per lane, unit 16n + lane%16 and row
-  // 16m + 4(lane/16) + r.  Each SIMD (waves s and s+4) takes IPS consecutive
-  // items, its first wave the first half; the last wave polls the barrier
-  // and takes none, so wave 3 takes all of SIMD 3's.
-  constexpr int NI = MT * NTU * 4, IPS = (NI + 3) / 4;
+  // 16m + 4(lane/16) + r.  The last wave polls the barrier and takes none;
+  // a wave's items run as one dependent chain (the phase is bound by its
+  // latency, not by the SIMD's issue rate), so no wave takes more than
+  // IPS = ceil(NI / 7): waves 0-3 (one per SIMD) IPS each, waves 4-6 the
+  // rest, evenly (12 items: 2, 2, 2, 2 and 2, 1, 1).
+  constexpr int NI = MT * NTU * 4, IPS = (NI + 6) / 7;
+  constexpr int FIRST = NI < 4 * IPS ? NI : 4 * IPS, REST = NI - FIRST;
   const int wv = __builtin_amdgcn_readfirstlane(wave);  // (scalar: the item indices are wave-uniform)
-  const int simd = wv & 3, s_lo = min(NI, simd * IPS), s_hi = min(NI, s_lo + IPS);
-  const int s_mid = simd == 3 ? s_hi : min(s_hi, s_lo + (IPS + 1) / 2);
-  const int i_lo = wv < 4 ? s_lo : s_mid, i_hi = wv < 4 ? s_mid : (wv == 7 ? s_mid : s_hi);
+  int i_lo, i_hi;
+  if (wv < 4) {
+    i_lo = min(NI, wv * IPS);
+    i_hi = min(FIRST, i_lo + IPS);
+  } else if (wv < 7) {
+    const int w = wv - 4;
+    i_lo = FIRST + w * (REST / 3) + min(w, REST % 3);
+    i_hi = i_lo + REST / 3 + (w < REST % 3 ? 1 : 0);
+  } else {
+    i_lo = i_hi = NI;
+  }
   const int nitems = i_hi - i_lo;  // at most IPS
   auto item_m = [&](int k) { return (i_lo + k) / (NTU * 4); };
   auto item_n = [&](int k) { return ((i_lo + k) / 4) % NTU; };
