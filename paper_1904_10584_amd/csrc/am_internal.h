@@ -208,6 +208,14 @@ hipError_t sgd_apply_f32(int64_t n, float* master, uint16_t* w_bf16, const float
 hipError_t cast_f32_bf16(int64_t n, const float* src, uint16_t* dst, hipStream_t s);
 // dst[c][r] = src[r][c] for a rows x cols matrix of the activation type.
 hipError_t transpose(const void* src, void* dst, int rows, int cols, bool bf16, hipStream_t s);
+// Up to MAX bf16 matrices of one shape (rows, cols multiples of 8, 16-byte
+// aligned) transposed in one launch; hipErrorInvalidValue if they are not.
+struct TransposeBatch {
+  static constexpr int MAX = 8;
+  const void* src[MAX];
+  void* dst[MAX];
+};
+hipError_t transpose_bf16_batch(const TransposeBatch& tb, int n, int rows, int cols, hipStream_t s);
 // out[c] = sum_r in[r][c] (fp32 result, fixed summation order).
 hipError_t colsum(const void* in, int64_t rows, int cols, bool bf16, float* out,
                   float* ws_partial, int n_chunks, hipStream_t s);

@@ -247,7 +247,7 @@ WsLayout ws_layout(const am_model* m, int64_t B, int64_t N) {
   }
   w.p_da = take(N * G * e);
   w.dh = take(N * H * e);
-  w.wht = take(G * H * e);
+  w.wht = take(L * G * H * e);  // W_h^T of every layer (transposed in one launch)
   w.dc = take(B * H * 4);
   w.c0 = take(L * B * H * 4);
   w.h0 = take(L * B * H * e);
@@ -917,9 +917,30 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
                           (int)H, (int)Cc, bf), s));
 
   char* dA = at<char>(ws, w.p_da);
-  void* WhT = at<void>(ws, w.wht);
+  auto wht = [&](int l) { return static_cast<void*>(at<char>(ws, w.wht) + (int64_t)l * G * H * e); };
   float* dc = at<float>(ws, w.dc);
+  // the XCD-local recurrences read W_h^T: every layer's, transposed up front
+  // in one launch (falls back to one transpose per layer below)
+  bool wht_ready = false;
+  if (sc.N > 0 && persistent_enabled() && bf && xcd_enabled() &&
+      am::lstm_xcd_instantiated(false, (int)H, B)) {
+    Timed tm(AM_K_MISC, s, 0.0, 2.0 * L * G * H * e);
+    wht_ready = true;
+    for (int l0 = 0; l0 < L && wht_ready; l0 += am::TransposeBatch::MAX) {
+      am::TransposeBatch tb{};
+      const int n = (int)(L - l0 < am::TransposeBatch::MAX ? L - l0 : am::TransposeBatch::MAX);
+      for (int i = 0; i < n; ++i) {
+        tb.src[i] = P8 + po.wh[l0 + i] * e;
+        tb.dst[i] = wht(l0 + i);
+      }
+      const hipError_t err = am::transpose_bf16_batch(tb, n, (int)G, (int)H, s);
+      if (err == hipErrorInvalidValue) wht_ready = false;  // (alignment) per layer instead
+      else AM_TRY(hip_check(err, "Wh transposes"));
+    }
+    if (!wht_ready) tm.cancel();
+  }
   for (int l = L - 1; l >= 0; --l) {
+    void* WhT = wht(l);
     const int64_t D = l == 0 ? m->input_dim : H;
     const char* Gl = at<char>(ws, w.g[l]);
     const float* Cl = at<float>(ws, w.c[l]);
@@ -941,7 +962,7 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
       const double flops = 2.0 * (sc.N - sc.counts[0]) * G * H;
       const double bytes = (double)sc.N * (G * e * 2 + H * (e + 8)) + (double)G * H * e;
       if (bf && xcd_enabled() && am::lstm_xcd_instantiated(false, (int)H, B)) {
-        {
+        if (!wht_ready) {
           Timed tm(AM_K_MISC, s, 0.0, 2.0 * G * H * e);
           AM_TRY(hip_check(am::transpose(P8 + po.wh[l] * e, WhT, (int)G, (int)H, bf, s), "Wh transpose"));
         }

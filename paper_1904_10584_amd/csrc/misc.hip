@@ -99,9 +99,10 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ sr
 // through LDS.  Thread (column, row chunk) gathers eight rows of one column.
 // The chunks of tile row i sit XOR-permuted by (i / 8) % 8, so the eight
 // rows 8 apart that the lanes of one read touch fall in different banks.
-__global__ __launch_bounds__(256) void transpose_bf16_x8(const bf16_t* __restrict__ src,
-                                                         bf16_t* __restrict__ dst, int rows,
-                                                         int cols) {
+// Several matrices of one shape in one launch: blockIdx.z picks the pair.
+__global__ __launch_bounds__(256) void transpose_bf16_x8(TransposeBatch tb, int rows, int cols) {
+  const bf16_t* __restrict__ src = static_cast<const bf16_t*>(tb.src[blockIdx.z]);
+  bf16_t* __restrict__ dst = static_cast<bf16_t*>(tb.dst[blockIdx.z]);
   __shared__ __align__(16) bf16_t tile[64 * 64];
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
   auto at = [](int i, int j) { return i * 64 + (((j >> 3) ^ ((i >> 3) & 7)) << 3) + (j & 7); };
@@ -225,9 +226,24 @@ hipError_t transpose(const void* src, void* dst, int rows, int cols, bool bf16, 
   dim3 grid((cols + 63) / 64, (rows + 63) / 64);
   const bool x8 = rows % 8 == 0 && cols % 8 == 0 &&
                   ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15) == 0;
-  if (bf16 && x8) hipLaunchKernelGGL(transpose_bf16_x8, grid, dim3(256), 0, s, (const bf16_t*)src, (bf16_t*)dst, rows, cols);
+  if (bf16 && x8) {
+    TransposeBatch tb{};
+    tb.src[0] = src;
+    tb.dst[0] = dst;
+    hipLaunchKernelGGL(transpose_bf16_x8, grid, dim3(256), 0, s, tb, rows, cols);
+  }
   else if (bf16) hipLaunchKernelGGL(transpose_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)src, (bf16_t*)dst, rows, cols);
   else hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(256), 0, s, (const float*)src, (float*)dst, rows, cols);
+  return hipGetLastError();
+}
+
+hipError_t transpose_bf16_batch(const TransposeBatch& tb, int n, int rows, int cols, hipStream_t s) {
+  if (n <= 0 || n > TransposeBatch::MAX || rows % 8 != 0 || cols % 8 != 0) return hipErrorInvalidValue;
+  for (int i = 0; i < n; ++i)
+    if (((reinterpret_cast<uintptr_t>(tb.src[i]) | reinterpret_cast<uintptr_t>(tb.dst[i])) & 15) != 0)
+      return hipErrorInvalidValue;
+  hipLaunchKernelGGL(transpose_bf16_x8, dim3((cols + 63) / 64, (rows + 63) / 64, n), dim3(256), 0, s,
+                     tb, rows, cols);
   return hipGetLastError();
 }
 
