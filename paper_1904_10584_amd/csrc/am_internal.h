@@ -221,6 +221,7 @@ hipError_t colsum(const void* in, int64_t rows, int cols, bool bf16, float* out,
                   float* ws_partial, int n_chunks, hipStream_t s);
 // dst[0..n) = +0.0 (a kernel, so the call is safe inside graph capture).
 hipError_t fill_zero(float* dst, int64_t n, hipStream_t s);
+hipError_t fill_zero2(float* d0, int64_t n0, float* d1, int64_t n1, hipStream_t s);
 // Convert fp32 [rows][cols] to the activation type (h0 for the recurrence).
 hipError_t convert_rows(const float* src, void* dst, int64_t count, bool bf16, hipStream_t s);
 // Final states: out[b][j] = state at row[b] (or init[b][j] / 0 if row[b] < 0).

@@ -700,8 +700,8 @@ am_status blstm_teacher_forward(const am_model* m, const void* params, const voi
     st.lens = at<int32_t>(ws, w.lens);
     AM_TRY(hip_check(am::schedule_tables(st, s), "schedule tables"));
   }
-  AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.c0), B * H, s), "c0 clear"));
-  AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), 2 * L * SYNC_BYTES / 4, s), "sync clear"));
+  AM_TRY(hip_check(am::fill_zero2(at<float>(ws, w.c0), B * H, at<float>(ws, w.sync),
+                                  2 * L * SYNC_BYTES / 4, s), "c0 and sync clear"));
   auto gather = [&](const void* src, int64_t src_ld, void* dst, int64_t dst_ld, int64_t col,
                     int width, bool reverse) {
     am::GatherRows g;
@@ -822,11 +822,11 @@ am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
     Timed tm(AM_K_MISC, s, 0.0, 8.0 * L * B * H);
     float* c0w = at<float>(ws, w.c0);
     if (c0) AM_TRY(hip_check(am::convert_rows(c0, c0w, L * B * H, false, s), "c0 copy"));
-    else AM_TRY(hip_check(am::fill_zero(c0w, L * B * H, s), "c0 clear"));
     if (h0) AM_TRY(hip_check(am::convert_rows(h0, at<void>(ws, w.h0), L * B * H, bf, s), "h0 convert"));
     // a new forward + backward pair: every slot of the sync area and the
-    // barrier time-out flag
-    AM_TRY(hip_check(am::fill_zero(at<float>(ws, w.sync), 2 * L * SYNC_BYTES / 4, s), "sync clear"));
+    // barrier time-out flag (and a zero initial cell state, in the same launch)
+    AM_TRY(hip_check(am::fill_zero2(at<float>(ws, w.sync), 2 * L * SYNC_BYTES / 4, c0w,
+                                    c0 ? 0 : L * B * H, s), "sync and c0 clear"));
   }
 
   for (int l = 0; l < L; ++l) {

@@ -64,9 +64,13 @@ __global__ __launch_bounds__(256) void cast_kernel(int64_t n, const float* __res
   }
 }
 
-__global__ __launch_bounds__(256) void fill_zero_kernel(int64_t n, float* __restrict__ dst) {
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
-    dst[i] = 0.f;
+// Zero n0 floats at d0, then n1 at d1 (one launch for two ranges).
+__global__ __launch_bounds__(256) void fill_zero_kernel(int64_t n0, float* __restrict__ d0, int64_t n1,
+                                                        float* __restrict__ d1) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n0 + n1; i += (int64_t)gridDim.x * 256) {
+    if (i < n0) d0[i] = 0.f;
+    else d1[i - n0] = 0.f;
+  }
 }
 
 template <typename T>
@@ -218,7 +222,12 @@ hipError_t convert_rows(const float* src, void* dst, int64_t count, bool bf16, h
 
 hipError_t fill_zero(float* dst, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(n, 256)), dim3(256), 0, s, n, dst);
+  return fill_zero2(dst, n, nullptr, 0, s);
+}
+
+hipError_t fill_zero2(float* d0, int64_t n0, float* d1, int64_t n1, hipStream_t s) {
+  if (n0 + n1 == 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(n0 + n1, 256)), dim3(256), 0, s, n0, d0, n1, d1);
   return hipGetLastError();
 }
 
