@@ -21,7 +21,9 @@
  *  - Arguments are validated on the host before anything is enqueued; on any
  *    error nothing is enqueued and no buffer is touched.  The return value is
  *    an am_status; am_last_error() gives a message for the calling thread.
- *  - Values inside device buffers (target indices, counts) are not checked.
+ *  - Values inside device buffers (target indices, counts) are not checked,
+ *    except that with AM_DEBUG=1 in the environment sparse_soft_ce
+ *    synchronises its stream and checks every target index (see there).
  *
  * Model and tensor layouts:
  *  - am_model { layers L, input_dim D0, hidden H, classes C, dtype }.
@@ -92,6 +94,22 @@ int64_t am_encode_workspace_bytes(int64_t n);
 const char* am_status_string(int32_t status);
 const char* am_last_error(void);
 
+/* Which kernels run one layer's recurrence (forward = 1: the forward pass;
+ * 0: BPTT) for a batch of B sequences and T steps (varlen = 1 if their
+ * lengths differ), as lstm_am_forward / lstm_am_backward choose them:
+ *   AM_PATH_XCD    one persistent launch per layer whose blocks of sequences
+ *                  each exchange state inside one XCD's L2 (bf16, shapes the
+ *                  kernels are built for; variable lengths need T <= 65535);
+ *   AM_PATH_DEVICE one persistent launch per layer with a device-scope
+ *                  exchange (its grid checked against the current device's
+ *                  occupancy: never chosen without a device);
+ *   AM_PATH_STEP   one launch per time step.
+ * A persistent grid that cannot be resident at launch falls back to the
+ * next path.  -1 if the model or sizes are invalid.  Host only. */
+enum { AM_PATH_XCD = 1, AM_PATH_DEVICE = 2, AM_PATH_STEP = 3 };
+int32_t am_recurrence_path(const am_model* m, int32_t T, int32_t B, int32_t varlen,
+                           int32_t forward);
+
 /* ---- the training step ------------------------------------------------- */
 
 /* Forward pass of the student LSTM acoustic model (§II-B): per layer and
@@ -114,9 +132,12 @@ am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
  *   loss_f = -sum_j p_fj (z_{f,idx_fj} - logsumexp(z_f)),  M_f = sum_j p_fj,
  *   dlogits_f = s_f (M_f softmax(z_f) - sum_j p_fj e_{idx_fj}),
  *   loss = sum_f s_f loss_f,  s_f = m_f / sum(m) (AM_MEAN_VALID) or m_f (AM_SUM).
- * Targets are used as given (no renormalisation); idx -1 marks an empty slot
- * (any index outside [0, C) is treated as empty); repeated indices add.  Rows
- * with m_f = 0 get zero gradient and their logits are not read.
+ * Targets are used as given (no renormalisation); idx -1 marks an empty slot;
+ * repeated indices add.  An index outside [-1, C) is a caller error: release
+ * builds treat it as an empty slot; with AM_DEBUG=1 in the environment the
+ * call synchronises `stream` (after the work queued before it), checks every
+ * index of idx and returns AM_EINVAL, with nothing enqueued, if one is out of
+ * range.  Rows with m_f = 0 get zero gradient and their logits are not read.
  * Requirements: C % 4 == 0, C <= 8192, logits 16-byte aligned.
  *   logits [N][C] fp32;  idx [N][K] int32;  prob [N][K] fp32
  *   mask   [N] uint8 or NULL (all valid);  loss [1] fp32 (written)
@@ -142,7 +163,11 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
  * and a wait that runs out (workgroups not co-resident, a stalled device)
  * sets a flag in `ws` instead of hanging.  Synchronises `stream`, then
  * returns AM_OK, or AM_ETIMEOUT when the flag is set (the outputs of that
- * pass must be discarded).  The flag is cleared by the next forward call. */
+ * pass must be discarded).  The flag is cleared by the next forward call.
+ * lstm_am_backward reads the flag on the device as its last step and, when
+ * it is set, overwrites `grads` with zeros, so that a caller that encodes
+ * and applies the gradient before this check adds nothing to its residual
+ * or weights. */
 am_status am_workspace_check(const void* ws, int64_t ws_bytes, void* stream);
 
 /* Gradient Threshold Compression encode (§VI-A), exact fp32:
@@ -262,7 +287,7 @@ am_status grad_threshold_decode_multi(int32_t streams, const uint32_t* words, in
                                       int32_t accumulate, void* ws, int64_t ws_bytes,
                                       void* stream);
 
-/* BMUF-NBM global step that ends a block of local SGD (§VI-B, eqs. (1)-(4)),
+/* BMUF-NBM global step that ends a block of local SGD (§VI-B, eqs. (2)-(5)),
  * per element i, in fp64 from the fp32 inputs, in this order, without fused
  * multiply-adds, each output rounded once to fp32:
  *   Wbar  = (models[0][i] + models[1][i] + ... + models[count-1][i]) / workers
@@ -273,7 +298,7 @@ am_status grad_threshold_decode_multi(int32_t streams, const uint32_t* words, in
  *   local_master[i] = W (or NULL);  local_bf16[i] = RNE bf16 of W (or NULL).
  * models: `count` fp32 rows `model_stride` elements apart: the N local
  * models (count = workers = N), or their all-reduced sum (count = 1,
- * workers = N).  Eq. (5) sets zeta = C N (1 - eta) for a constant C >= 1.
+ * workers = N).  Eq. (6) sets zeta = C N (1 - eta) for a constant C >= 1.
  * Each output may alias an input at the same index (in-place state, or the
  * restart copy written over an addend).                                    */
 am_status bmuf_block_update(int64_t n, int32_t count, int32_t workers, const float* models,

@@ -21,7 +21,7 @@ What it computes, in the order the training step runs it
   feedback, +-tau one-bit quantisation and 32-bit index/sign packing, the
   matching decode, and the aggregate of several workers' sparse updates.
 * ``bmuf``     -- the BMUF-NBM global step that ends a block of local SGD
-  (§VI-B, eqs. (1)-(5)).
+  (§VI-B, eqs. (2)-(6)).
 * ``features`` -- the student's input frames (three 10 ms frames stacked at a
   30 ms advance, causal mean subtraction, global normalisation) and the
   targets delayed by the model's look-ahead (§II-B).

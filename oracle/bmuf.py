@@ -1,5 +1,5 @@
 """Blockwise model update filtering with Nesterov block momentum (BMUF-NBM),
-the global step that ends every block of local SGD (§VI-B, eqs. (1)-(5)).
+the global step that ends every block of local SGD (§VI-B, eqs. (2)-(6)).
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
@@ -7,23 +7,25 @@ Each of N workers trains its own copy W^i of the model with mini-batch SGD
 for a block of mini-batches; the global model W_g then moves as follows,
 written in the paper's notation:
 
-    (1)  Wbar(t)  = (1/N) sum_i W(t)^i             model average
-    (2)  G(t)     = Wbar(t) - W_g(t-1)             block-level update
-    (3)  Delta(t) = eta_t Delta(t-1) + zeta_t G(t) block momentum
-    (4)  W_g(t)   = W_g(t-1) + Delta(t) + eta_{t+1} Delta(t)
+    (2)  Wbar(t)  = (1/N) sum_i W(t)^i             model average
+    (3)  G(t)     = Wbar(t) - W_g(t-1)             block-level update
+    (4)  Delta(t) = eta_t Delta(t-1) + zeta_t G(t) block momentum
+    (5)  W_g(t)   = W_g(t-1) + Delta(t) + eta_{t+1} Delta(t)
                                                    Nesterov look-ahead
-    (5)  zeta / (N (1 - eta)) = C, C >= 1          how eta and zeta are set
+    (6)  zeta / (N (1 - eta)) = C, C >= 1          how eta and zeta are set
+
+(the paper's numbering: its eq. (1) is the decoding rule of the recogniser)
 
 Readings (the paper gives the equations, not their arithmetic):
-  * eq. (4) is taken literally, as printed: W_g(t) is the model broadcast to
+  * eq. (5) is taken literally, as printed: W_g(t) is the model broadcast to
     the workers for the next block, one line that adds Delta(t) and the
     look-ahead eta_{t+1} Delta(t) to W_g(t-1);
   * the model average may arrive as the N models (one GPU holding them) or
     already summed by an all-reduce: ``count`` addends are summed and the sum
     is divided by ``workers``;
-  * W_g and Delta are fp32 state; each step evaluates (1)-(4) in fp64 from the
-    fp32 inputs, in the order written (the sum of (1) left to right over the
-    addends, then the division; (3) and (4) left to right with no fused
+  * W_g and Delta are fp32 state; each step evaluates (2)-(5) in fp64 from the
+    fp32 inputs, in the order written (the sum of (2) left to right over the
+    addends, then the division; (4) and (5) left to right with no fused
     multiply-add), and rounds once to fp32 per output;
   * the workers restart from W_g(t); its bf16 working copy is the
     round-to-nearest-even image of the new fp32 value.
@@ -35,7 +37,7 @@ from .numerics import bf16_bits
 
 
 def bmuf_zeta(C, workers, eta):
-    """Block learning rate from eq. (5): zeta = C N (1 - eta)."""
+    """Block learning rate from eq. (6): zeta = C N (1 - eta)."""
     return float(C) * float(workers) * (1.0 - float(eta))
 
 
@@ -59,11 +61,11 @@ def bmuf_block_update(models, workers, global_w, delta, eta, eta_next, zeta):
     eta_next = np.float64(np.float32(eta_next))
     zeta = np.float64(np.float32(zeta))
     s = np.zeros_like(wg)
-    for i in range(m.shape[0]):                    # (1): fixed order
+    for i in range(m.shape[0]):                    # (2): fixed order
         s = s + m[i].astype(np.float64)
     wbar = s / np.float64(workers)
-    g = wbar - wg                                  # (2)
-    d = eta * d0 + zeta * g                        # (3)
-    new_w = (wg + d) + eta_next * d                # (4)
+    g = wbar - wg                                  # (3)
+    d = eta * d0 + zeta * g                        # (4)
+    new_w = (wg + d) + eta_next * d                # (5)
     new_w32 = new_w.astype(np.float32)
     return new_w32, d.astype(np.float32), bf16_bits(new_w32)

@@ -24,8 +24,16 @@ KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd_data", "gemm_bwd_wgt", "lstm_fwd", "lstm
                   "soft_ce", "encode", "decode", "sgd", "misc", "bmuf"]
 
 
+OK, EINVAL, ECAPACITY, EUNSUPPORTED, EHIP, EWORKSPACE, ETIMEOUT = 0, -1, -2, -3, -4, -5, -6
+PATH_XCD, PATH_DEVICE, PATH_STEP = 1, 2, 3
+
+
 class AmError(RuntimeError):
-    pass
+    """A non-OK am_status (``status``), with the library's message."""
+
+    def __init__(self, msg, status=None):
+        super().__init__(msg)
+        self.status = status
 
 
 class _Model(ctypes.Structure):
@@ -59,6 +67,7 @@ _PROTOS = {
     "am_ce_workspace_bytes": (_I64, [_I64]),
     "am_encode_workspace_bytes": (_I64, [_I64]),
     "am_status_string": (ctypes.c_char_p, [_I32]),
+    "am_recurrence_path": (_I32, [_P, _I32, _I32, _I32, _I32]),
     "am_last_error": (ctypes.c_char_p, []),
     "lstm_am_forward": (_I32, [_P, _P, _P, _P, _P, _P, _I32, _I32, _P, _P, _P, _P, _I64, _P]),
     "sparse_soft_ce": (_I32, [_I64, _I32, _I32, _P, _P, _P, _P, _I32, _P, _P, _I32, _P, _I64, _P]),
@@ -110,7 +119,7 @@ def _check(status):
     if status != 0:
         L = lib()
         raise AmError(f"{L.am_status_string(status).decode()} ({status}): "
-                      f"{L.am_last_error().decode()}")
+                      f"{L.am_last_error().decode()}", status)
 
 
 def _dev(t, name, dtype=None):
@@ -159,6 +168,15 @@ def workspace_bytes(m: Model, T, B, N) -> int:
     if n < 0:
         raise AmError("invalid model or batch for workspace query")
     return int(n)
+
+
+def recurrence_path(m: Model, T, B, varlen=False, forward=True) -> int:
+    """PATH_XCD, PATH_DEVICE or PATH_STEP: the kernels a layer's recurrence
+    takes for this batch shape (see am_recurrence_path)."""
+    p = lib().am_recurrence_path(ctypes.byref(m.c()), T, B, 1 if varlen else 0, 1 if forward else 0)
+    if p < 0:
+        raise AmError("invalid model or batch for the recurrence-path query", EINVAL)
+    return int(p)
 
 
 def ce_workspace_bytes(N) -> int:

@@ -110,7 +110,9 @@ struct XcdSync {
   unsigned* flags;  // a 32-word line per block of sequences, a word per member
   int* xcc;         // the same for the members' XCD ids (check of the layout)
   int* err;
-  int units;  // filled in by the launcher
+  int units;   // filled in by the launcher
+  int fenced;  // nonzero: exchange with release/acquire fences even when every
+               // block is found on one XCD (AM_XCD_FENCED=1, for tests)
 };
 bool lstm_xcd_instantiated(bool forward, int hidden, int B);
 // Launch of a grid that the caller has checked fits on the device at once
@@ -222,6 +224,8 @@ hipError_t colsum(const void* in, int64_t rows, int cols, bool bf16, float* out,
 // dst[0..n) = +0.0 (a kernel, so the call is safe inside graph capture).
 hipError_t fill_zero(float* dst, int64_t n, hipStream_t s);
 hipError_t fill_zero2(float* d0, int64_t n0, float* d1, int64_t n1, hipStream_t s);
+// dst[0..n) = +0.0 when *flag (device) is nonzero, else nothing.
+hipError_t zero_if_set(const int* flag, float* dst, int64_t n, hipStream_t s);
 // Convert fp32 [rows][cols] to the activation type (h0 for the recurrence).
 hipError_t convert_rows(const float* src, void* dst, int64_t count, bool bf16, hipStream_t s);
 // Final states: out[b][j] = state at row[b] (or init[b][j] / 0 if row[b] < 0).

@@ -204,9 +204,30 @@ am::XcdSync xcd_sync(void* slot, int* err) {
   y.xcc = reinterpret_cast<int*>(u + 512);  // XCC line of block k: u[512 + 32 k ..], the same
   y.err = err;
   y.units = 0;
+  y.fenced = 0;
   return y;
 }
 static_assert(512 + 512 <= SYNC_STICKY_WORD, "a slot holds the flag and XCC lines below the time-out word");
+
+// Whether the XCD-local kernels take this layer's recurrence: bf16, the
+// shape instantiated, and (variable lengths) T within the schedule's 16-bit
+// lengths.
+bool xcd_shape(bool forward, bool bf, int64_t H, int T, int B, bool varlen) {
+  return bf && xcd_enabled() && am::lstm_xcd_instantiated(forward, (int)H, B) &&
+         (!varlen || T <= 65535);
+}
+bool xcd_path(bool forward, bool bf, int64_t H, const Schedule& sc) {
+  bool varlen = false;
+  for (int b = 0; b < sc.B && !varlen; ++b) varlen = sc.lens[b] != sc.T;
+  return xcd_shape(forward, bf, H, sc.T, sc.B, varlen);
+}
+
+// AM_DEBUG=1 in the environment: entry points that consume indices held in
+// device buffers synchronise and check them.
+bool debug_checks() {
+  const char* v = getenv("AM_DEBUG");
+  return v && v[0] == '1' && v[1] == 0;
+}
 
 am::PersistSchedule persist_schedule(const Schedule& sc) {
   am::PersistSchedule ps;
@@ -296,7 +317,7 @@ am_status forward_recurrence(const FwdLayer& f, const Schedule& sc, bool bf, int
     const double flops = 2.0 * sc.N * G * H;
     const double bytes = (double)sc.N * (G * e * 2 + H * (2 * e + 4)) + (double)G * H * e;
     bool used = false;
-    if (bf && xcd_enabled() && am::lstm_xcd_instantiated(true, (int)H, B)) {
+    if (xcd_path(true, bf, H, sc)) {
       Timed tm(AM_K_LSTM_FWD, s, flops, bytes);
       AM_TRY(hip_check(am::lstm_fwd_xcd_launch(pa, ps, xcd_sync(f.sync, f.err), s, &used),
                        "lstm forward layer (xcd)"));
@@ -474,6 +495,17 @@ am_status am_param_offsets(const am_model* m, int64_t* offsets) {
   offsets[3 * m->layers] = o.wo;
   offsets[3 * m->layers + 1] = o.bo;
   return AM_OK;
+}
+
+int32_t am_recurrence_path(const am_model* m, int32_t T, int32_t B, int32_t varlen,
+                           int32_t forward) {
+  if (check_model(m) != AM_OK || T < 0 || B < 1) return -1;
+  const bool bf = m->dtype == AM_BF16, fw = forward != 0;
+  if (!persistent_enabled()) return AM_PATH_STEP;
+  if (xcd_shape(fw, bf, m->hidden, T, B, varlen != 0)) return AM_PATH_XCD;
+  if (device_persistent_enabled() && am::lstm_persistent_fits(fw, m->hidden, B, bf, T))
+    return AM_PATH_DEVICE;
+  return AM_PATH_STEP;
 }
 
 int64_t am_workspace_bytes(const am_model* m, int32_t T, int32_t B, int64_t N) {
@@ -785,6 +817,18 @@ am_status sparse_soft_ce(int64_t N, int32_t C, int32_t K, const float* logits, c
   if (!ws || ws_bytes < need || !aligned(ws, 256))
     return fail(AM_EWORKSPACE, "soft_ce needs %lld workspace bytes (256-aligned)", (long long)need);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (debug_checks() && N > 0 && K > 0) {
+    // every target index in [-1, C): copied to the host after the work
+    // queued before this call, then checked
+    std::vector<int32_t> h((size_t)(N * K));
+    AM_TRY(hip_check(hipMemcpyAsync(h.data(), idx, h.size() * 4, hipMemcpyDeviceToHost, s),
+                     "AM_DEBUG index copy"));
+    AM_TRY(hip_check(hipStreamSynchronize(s), "AM_DEBUG stream sync"));
+    for (size_t i = 0; i < h.size(); ++i)
+      if (h[i] < -1 || h[i] >= C)
+        return fail(AM_EINVAL, "target index %d of row %lld, slot %lld outside [-1, %d)", h[i],
+                    (long long)(i / K), (long long)(i % K), C);
+  }
   am::SoftCeArgs a;
   a.N = N; a.C = C; a.K = K; a.z = logits; a.idx = idx; a.prob = prob; a.mask = mask;
   a.reduction = reduction; a.loss = loss; a.dz = dlogits; a.dz_bf16 = dlogits_dtype == AM_BF16;
@@ -922,8 +966,7 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
   // the XCD-local recurrences read W_h^T: every layer's, transposed up front
   // in one launch (falls back to one transpose per layer below)
   bool wht_ready = false;
-  if (sc.N > 0 && persistent_enabled() && bf && xcd_enabled() &&
-      am::lstm_xcd_instantiated(false, (int)H, B)) {
+  if (sc.N > 0 && persistent_enabled() && xcd_path(false, bf, H, sc)) {
     Timed tm(AM_K_MISC, s, 0.0, 2.0 * L * G * H * e);
     wht_ready = true;
     for (int l0 = 0; l0 < L && wht_ready; l0 += am::TransposeBatch::MAX) {
@@ -961,7 +1004,7 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
       const am::PersistSchedule ps = persist_schedule(sc);
       const double flops = 2.0 * (sc.N - sc.counts[0]) * G * H;
       const double bytes = (double)sc.N * (G * e * 2 + H * (e + 8)) + (double)G * H * e;
-      if (bf && xcd_enabled() && am::lstm_xcd_instantiated(false, (int)H, B)) {
+      if (xcd_path(false, bf, H, sc)) {
         if (!wht_ready) {
           Timed tm(AM_K_MISC, s, 0.0, 2.0 * G * H * e);
           AM_TRY(hip_check(am::transpose(P8 + po.wh[l] * e, WhT, (int)G, (int)H, bf, s), "Wh transpose"));
@@ -1015,7 +1058,12 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
                       mk_gemm(dA, G, true, P8 + po.wx[l] * e, D, false, DH, H, false, nullptr, N,
                               (int)H, (int)G, bf), s));
   }
-  return AM_OK;
+  // a step barrier of this forward + backward pair that timed out leaves the
+  // gradient invalid: it is replaced by zeros on the device, so that a caller
+  // that encodes and applies it before am_workspace_check adds nothing to
+  // its residual or weights
+  Timed tm(AM_K_MISC, s, 0.0, 4.0);
+  return hip_check(am::zero_if_set(sync_err(at<void>(ws, w.sync)), grads, po.n, s), "time-out guard");
 }
 
 // ---------------------------------------------------------------- timing --

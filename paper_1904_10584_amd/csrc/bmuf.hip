@@ -1,9 +1,9 @@
 // BMUF-NBM global step (blockwise model update filtering with Nesterov block
-// momentum, §VI-B eqs. (1)-(4)), one HBM-bound pass over the flat model:
-//   Wbar  = (sum of the `count` addends) / workers       (1)
-//   G     = Wbar - W_g                                   (2)
-//   Delta = eta Delta + zeta G                           (3)
-//   W_g   = W_g + Delta + eta_next Delta                 (4)
+// momentum, §VI-B eqs. (2)-(5)), one HBM-bound pass over the flat model:
+//   Wbar  = (sum of the `count` addends) / workers       (2)
+//   G     = Wbar - W_g                                   (3)
+//   Delta = eta Delta + zeta G                           (4)
+//   W_g   = W_g + Delta + eta_next Delta                 (5)
 // and, optionally, the restart copy of the local model (fp32 and bf16).
 // Each element is evaluated in fp64 from its fp32 inputs, in the order
 // written, with no fused multiply-add, and each output is rounded once to

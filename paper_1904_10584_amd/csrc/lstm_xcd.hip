@@ -47,7 +47,8 @@ __device__ __forceinline__ unsigned xcc_id() {
 // of the block's line, and one wave waits for all members and compares.
 // Only the block's members take part, with plain device-scope loads and
 // stores: no read-modify-write, no cache write-back or invalidation.  Every
-// member of a block returns the same answer.
+// member of a block returns the same answer; y.fenced forces the fenced
+// exchange regardless (so that tests can run it).
 __device__ bool check_local(const XcdSync& y, int blk, int us, int members, int* bad_sh) {
   unsigned* line = reinterpret_cast<unsigned*>(y.xcc) + blk * 32;
   if (threadIdx.x < 64) {
@@ -65,7 +66,7 @@ __device__ bool check_local(const XcdSync& y, int blk, int us, int members, int*
     }
     const unsigned first = __shfl(v, 0, 64);
     const bool bad = __any(lane < members && v != first);
-    if (lane == 0) *bad_sh = bad ? 1 : 0;
+    if (lane == 0) *bad_sh = bad || y.fenced ? 1 : 0;
   }
   __syncthreads();
   return *bad_sh == 0;
@@ -677,11 +678,19 @@ XShape xshape(int H, int B) {
   if (x.MT == MT_ && x.KS == KS_ && x.TPW == TPW_ && (x.U % 8 == 0) == STG_)             \
     return coop(lstm_fwd_xcd<MT_, KS_, TPW_, STG_>, blocks, 512, lds, args, s, used);
 
+// AM_XCD_FENCED=1 in the environment: exchange with fences (as a block that
+// spans XCDs does) even when every block sits on one XCD.
+bool fenced_forced() {
+  const char* e = getenv("AM_XCD_FENCED");
+  return e && e[0] == '1' && e[1] == 0;
+}
+
 hipError_t lstm_fwd_xcd_launch(PersistFwd a, PersistSchedule ps, XcdSync y, hipStream_t s, bool* used) {
   *used = false;
   const XShape x = xshape(a.hidden, ps.B);
   if (!x.ok) return hipSuccess;
   y.units = x.U;
+  y.fenced = fenced_forced() ? 1 : 0;
   const int blocks = NX * x.BPX * (a.hidden / x.U);
   // h rows, partial tiles, and (U % 8 == 0) the staged rows of C, Hs and G
   const size_t lds = (size_t)16 * x.MT * x.KS * 64 + 8 * x.TPW * 64 * 16 +
@@ -705,6 +714,7 @@ hipError_t lstm_bwd_xcd_launch(PersistBwd a, PersistSchedule ps, XcdSync y, hipS
   const XShape x = xshape(a.hidden, ps.B);
   if (!x.ok) return hipSuccess;
   y.units = x.U;
+  y.fenced = fenced_forced() ? 1 : 0;
   const int blocks = NX * x.BPX * (a.hidden / x.U);
   // two private chunk buffers per wave, or the partial products if larger
   const int ch = x.KW >= 4 ? 4 : x.KW;

@@ -73,6 +73,14 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(int64_t n0, float* __res
   }
 }
 
+// dst[0..n) = +0.0 if *flag is nonzero; otherwise nothing (one workgroup:
+// the cheap case is the common one).
+__global__ __launch_bounds__(256) void zero_if_set_kernel(const int* __restrict__ flag, int64_t n,
+                                                          float* __restrict__ dst) {
+  if (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) return;
+  for (int64_t i = threadIdx.x; i < n; i += 256) dst[i] = 0.f;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void convert_kernel(int64_t n, const float* __restrict__ src,
                                                       T* __restrict__ dst) {
@@ -228,6 +236,12 @@ hipError_t fill_zero(float* dst, int64_t n, hipStream_t s) {
 hipError_t fill_zero2(float* d0, int64_t n0, float* d1, int64_t n1, hipStream_t s) {
   if (n0 + n1 == 0) return hipSuccess;
   hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(n0 + n1, 256)), dim3(256), 0, s, n0, d0, n1, d1);
+  return hipGetLastError();
+}
+
+hipError_t zero_if_set(const int* flag, float* dst, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_if_set_kernel, dim3(1), dim3(256), 0, s, flag, n, dst);
   return hipGetLastError();
 }
 

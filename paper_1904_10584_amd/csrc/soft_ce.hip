@@ -43,14 +43,19 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
   if (f < N) {
     const float* zr = z + f * C;
     DT* dr = dz + f * C;
-    // the row first, 16-byte loads issued back to back (a lane past C
-    // re-reads the row's start; its values are replaced below), so that
-    // the row costs one memory latency, not one per chunk
+    // with a mask, the row's mask byte first: a masked row's logits are
+    // never read (without one, no dependent load precedes the row)
+    const float m = mask ? (mask[f] != 0 ? 1.f : 0.f) : 1.f;
+    // the row, 16-byte loads issued back to back (a lane past C re-reads
+    // the row's start; its values are replaced below), so that the row
+    // costs one memory latency, not one per chunk
     float4 v[NCH];
+    if (m != 0.f) {
 #pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int c = i * 256 + lane * 4;
-      v[i] = *reinterpret_cast<const float4*>(zr + (c < C ? c : 0));
+      for (int i = 0; i < NCH; ++i) {
+        const int c = i * 256 + lane * 4;
+        v[i] = *reinterpret_cast<const float4*>(zr + (c < C ? c : 0));
+      }
     }
     // teacher entries: lane j holds entry j (K <= 64 per pass)
     const int32_t* ir = idx + f * K;
@@ -61,7 +66,6 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
       tc = ir[lane];
       tp = pr[lane];
     }
-    const float m = mask ? (mask[f] != 0 ? 1.f : 0.f) : 1.f;
     const float s = m * (scale_dev ? *scale_dev : scale_host);
     if (s == 0.f) {
 #pragma unroll

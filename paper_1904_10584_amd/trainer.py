@@ -5,6 +5,13 @@ BPTT (lstm_am_backward) -> [threshold encode of the gradient with residual
 error feedback -> decode] -> SGD on the fp32 master weights with a fresh bf16
 copy.  Every step runs on the current HIP stream without host
 synchronisation; this module only owns buffers and orders the calls.
+
+A recurrence whose step barrier timed out (its workgroups were not all
+resident, or the device stalled) leaves the pass invalid: lstm_am_backward
+then writes a zero gradient on the device, so a step that is encoded and
+applied before anyone looks adds nothing to the residual or the weights.
+check() synchronises and raises for such a pass; call it before relying on
+the loss or logits of a step.
 """
 
 import torch

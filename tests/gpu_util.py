@@ -1,6 +1,15 @@
 """Helpers for the GPU parity tests: run the HIP path through the C ABI on
-numpy inputs, run the oracle on the same inputs, and compare per tensor."""
+numpy inputs, run the oracle on the same inputs, and compare per tensor.
 
+Every float comparison applies two bounds to each tensor: the relative L2
+error ||x - ref|| / ||ref|| and the element-wise bound
+max|x - ref| <= tol * max|ref|, so that an error confined to one unit, one
+tile edge or one row of a large tensor cannot hide inside the norm.  With
+PARITY_LOG=<path> in the environment every comparison is appended to that
+file as a JSON line (test, tensor, both errors, tolerance)."""
+
+import json
+import os
 import sys
 
 import numpy as np
@@ -20,6 +29,44 @@ def rel_l2(a, ref):
     ref = np.asarray(ref, np.float64)
     den = np.linalg.norm(ref)
     return float(np.linalg.norm(a - ref) / den) if den > 0 else float(np.linalg.norm(a))
+
+
+def max_ratio(a, ref):
+    """max|a - ref| / max|ref| (element-wise error against the tensor's scale)."""
+    a = np.asarray(a, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if a.size == 0:
+        return 0.0
+    den = float(np.max(np.abs(ref)))
+    num = float(np.max(np.abs(a - ref)))
+    return num / den if den > 0 else num
+
+
+def _log(name, rl2, mr, tol):
+    path = os.environ.get("PARITY_LOG")
+    if not path:
+        return
+    test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
+    with open(path, "a") as fh:
+        fh.write(json.dumps({"test": test, "tensor": name, "rel_l2": rl2, "max_ratio": mr,
+                             "tol": tol}) + "\n")
+
+
+def assert_close(name, got, ref, tol):
+    """Both bounds on one tensor; returns (rel_l2, max_ratio)."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
+    rl2, mr = rel_l2(got, ref), max_ratio(got, ref)
+    _log(name, rl2, mr, tol)
+    assert rl2 <= tol, f"{name}: rel L2 {rl2:.3e} > {tol:g}"
+    if mr > tol:
+        i = int(np.argmax(np.abs(got - ref)))
+        where = np.unravel_index(i, ref.shape)
+        raise AssertionError(f"{name}: max|err| / max|ref| = {mr:.3e} > {tol:g} at {where} "
+                             f"(got {got.flat[i]!r}, ref {ref.flat[i]!r})")
+    return rl2, mr
 
 
 def to_dev(a, dtype=None):
@@ -96,6 +143,27 @@ def oracle_forward_backward(dims, master, x, T, B, idx, prob, lengths=None, h0=N
     out["dlogits"] = dz
     out["grads"] = oracle.lstm_am_backward(p, dims, cache, dz)
     return out
+
+
+def grad_tensors(grads, dims):
+    """Named parameter tensors of a flat gradient."""
+    gl, go = oracle.unpack_params(np.asarray(grads, np.float64), dims)
+    out = {"Wo": go["Wo"], "bo": go["bo"]}
+    for l, a in enumerate(gl):
+        for k in ("Wx", "Wh", "b"):
+            out[f"{k}{l}"] = a[k]
+    return out
+
+
+def check_grads(grads, ref, dims, tol, label="grad"):
+    """Both bounds on every parameter tensor of the gradient; returns the
+    largest rel L2 and the largest element-wise ratio."""
+    g, r = grad_tensors(grads, dims), grad_tensors(ref, dims)
+    worst_l2 = worst_mr = 0.0
+    for k in r:
+        rl2, mr = assert_close(f"{label}.{k}", g[k], r[k], tol)
+        worst_l2, worst_mr = max(worst_l2, rl2), max(worst_mr, mr)
+    return worst_l2, worst_mr
 
 
 def per_tensor_errors(grads, ref, dims):

@@ -195,3 +195,24 @@ def test_teacher_argument_checks(L):
     assert st == -3   # C > 8192
     st, _ = _status(L, "kbest_posteriors", -1, 20, fake, fake, None)
     assert st == -1
+
+
+def test_recurrence_path_query(monkeypatch):
+    # host logic only: the XCD-local kernels are built for bf16 H = 768 with
+    # B <= 256; variable lengths hold 16-bit lengths, so T > 65535 must not
+    # take them (the per-step kernels use the host's 64-bit schedule)
+    monkeypatch.delenv("AM_RECURRENCE", raising=False)
+    monkeypatch.delenv("AM_STEP_KERNELS", raising=False)
+    paper = am.Model(5, 192, 768, 3000, am.BF16)
+    for fwd in (True, False):
+        assert am.recurrence_path(paper, 64, 256, False, fwd) == am.PATH_XCD
+        assert am.recurrence_path(paper, 1500, 128, True, fwd) == am.PATH_XCD
+        assert am.recurrence_path(paper, 65535, 128, True, fwd) == am.PATH_XCD
+        assert am.recurrence_path(paper, 65536, 128, True, fwd) != am.PATH_XCD
+        assert am.recurrence_path(paper, 70000, 128, False, fwd) == am.PATH_XCD
+        # fp32 models never take the XCD-local kernels
+        assert am.recurrence_path(am.Model(5, 192, 768, 3000, am.F32), 64, 256, False, fwd) != am.PATH_XCD
+    monkeypatch.setenv("AM_RECURRENCE", "step")
+    assert am.recurrence_path(paper, 64, 256) == am.PATH_STEP
+    with pytest.raises(am.AmError):
+        am.recurrence_path(am.Model(5, 192, 770, 3000, am.BF16), 64, 256)

@@ -8,7 +8,7 @@ import torch
 
 import oracle
 from paper_1904_10584_amd import binding as am
-from tests.gpu_util import rel_l2, say, to_dev
+from tests.gpu_util import assert_close, say, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -162,12 +162,15 @@ def test_soft_ce_matches_oracle(N, C, K, opts, dz_bf16, reduction):
     got_dz = dz.float().cpu().numpy()
     assert abs(got_loss - ref_loss) <= 1e-5 * abs(ref_loss) + 1e-7
     tol = 4e-3 if dz_bf16 else 1e-5
-    assert rel_l2(got_dz, ref_dz) <= tol
+    assert_close("dlogits", got_dz, ref_dz, tol)
     if m is not None:
         assert np.all(got_dz[m == 0] == 0.0)
 
 
-def test_soft_ce_masked_rows_not_read():
+def test_soft_ce_masked_rows_ignore_their_logits():
+    # (the kernel reads a row's mask before its logits and loads no logit of
+    # a masked row; here the masked rows hold NaN, which must not reach the
+    # loss or any gradient row)
     N, C, K = 40, 512, 4
     z, idx, prob, _ = _ce_case(N, C, K, seed=3)
     m = np.ones(N, np.uint8)
@@ -182,3 +185,29 @@ def test_soft_ce_masked_rows_not_read():
     assert np.isfinite(float(loss.cpu()[0]))
     assert abs(float(loss.cpu()[0]) - ref_loss) <= 1e-5 * abs(ref_loss)
     assert np.all(np.isfinite(dz.cpu().numpy()))
+
+
+@pytest.mark.parametrize("bad", [3000, -2])
+def test_soft_ce_debug_mode_rejects_out_of_range_indices(bad, monkeypatch):
+    # AM_DEBUG=1: the call synchronises, finds the index outside [-1, C) and
+    # returns AM_EINVAL with nothing enqueued; without it the index is an
+    # empty slot
+    N, C, K = 64, 3000, 20
+    z, idx, prob, _ = _ce_case(N, C, K, seed=12)
+    idx[37, 11] = bad
+    dz = torch.full((N, C), 5.0, dtype=torch.float32, device="cuda")
+    loss = torch.full((1,), 5.0, dtype=torch.float32, device="cuda")
+    ws = torch.empty(am.ce_workspace_bytes(N), dtype=torch.uint8, device="cuda")
+    args = (to_dev(z), to_dev(idx), to_dev(prob), loss, dz, ws)
+    monkeypatch.setenv("AM_DEBUG", "1")
+    with pytest.raises(am.AmError) as ei:
+        am.sparse_soft_ce(*args)
+    assert ei.value.status == am.EINVAL
+    assert "row 37, slot 11" in str(ei.value)
+    torch.cuda.synchronize()
+    assert float(loss.cpu()[0]) == 5.0 and bool(torch.all(dz == 5.0))
+    monkeypatch.delenv("AM_DEBUG")
+    am.sparse_soft_ce(*args)
+    ref_loss, ref_dz = oracle.sparse_soft_ce(z, np.where((idx >= 0) & (idx < C), idx, -1), prob)
+    assert abs(float(loss.cpu()[0]) - ref_loss) <= 1e-5 * abs(ref_loss)
+    assert_close("dlogits", dz.cpu().numpy(), ref_dz, 1e-5)

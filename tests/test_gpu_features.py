@@ -11,7 +11,7 @@ import torch
 import oracle
 from paper_1904_10584_amd import binding as am
 from paper_1904_10584_amd import synth
-from tests.gpu_util import bf16_dev, per_tensor_errors, rel_l2, say, to_dev
+from tests.gpu_util import assert_close, bf16_dev, check_grads, say, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -166,6 +166,6 @@ def test_raw_frames_to_gradients_with_carried_state_and_delay():
     ref_loss, ref_dz = oracle.sparse_soft_ce(ref_logits, i_d, p_d, msk)
     ref_grads = oracle.lstm_am_backward(master, dims, cache, ref_dz)
     assert abs(float(loss.cpu()[0]) - ref_loss) <= 1e-4 * abs(ref_loss)
-    assert rel_l2(logits.cpu().numpy(), ref_logits) <= 1e-4
-    errs = per_tensor_errors(grads.cpu().numpy(), ref_grads, dims)
-    assert max(errs.values()) <= 1e-4, errs
+    assert_close("logits", logits.cpu().numpy(), ref_logits, 1e-4)
+    assert_close("dlogits", dz.cpu().numpy(), ref_dz, 1e-4)
+    check_grads(grads.cpu().numpy(), ref_grads, dims, 1e-4)

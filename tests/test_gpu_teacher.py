@@ -11,7 +11,7 @@ import torch
 import oracle
 from paper_1904_10584_amd import binding as am
 from paper_1904_10584_amd import synth
-from tests.gpu_util import bf16_dev, rel_l2, say, to_dev
+from tests.gpu_util import assert_close, bf16_dev, say, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -49,9 +49,8 @@ def test_teacher_small_matches_oracle(dtype, lengths_kind):
     p = oracle.bf16_round(master) if bf else master.astype(np.float32)
     xe = oracle.bf16_round(x) if bf else x
     ref = oracle.teacher_forward(p, d, xe, T, B, lengths)
-    err = rel_l2(got, ref)
-    say(f"  rel err {err:.2e}")
-    assert err <= (2e-2 if bf else 1e-4)
+    l2, mr = assert_close("teacher logits", got, ref, 2e-2 if bf else 1e-4)
+    say(f"  rel L2 {l2:.2e}, max element ratio {mr:.2e}")
 
 
 @pytest.mark.timeout(300)
@@ -66,12 +65,15 @@ def test_teacher_paper_scale_sampled_sequences():
     say(f"teacher 5x768 n={n}")
     got = _teacher_gpu(m, master, x, T, B)
     p = oracle.bf16_round(master)
-    for b in (0, 131, 255):
-        rows = np.arange(T) * B + b
-        ref = oracle.teacher_forward(p, d, oracle.bf16_round(x[rows]), T, 1)
-        err = rel_l2(got[rows], ref)
-        say(f"  sequence {b}: rel err {err:.2e}")
-        assert err <= 2e-2
+    # one sequence of every 16-sequence block (the recurrence serves the
+    # batch in such blocks, two per XCD), as one oracle batch
+    sample = [16 * k + k for k in range(B // 16)]
+    rows = (np.arange(T)[:, None] * B + np.array(sample)[None, :]).reshape(-1)
+    ref = oracle.teacher_forward(p, d, oracle.bf16_round(x[rows]), T, len(sample))
+    for i, b in enumerate(sample):
+        mine = np.arange(T) * len(sample) + i
+        l2, mr = assert_close(f"teacher logits(seq {b})", got[rows[mine]], ref[mine], 2e-2)
+        say(f"  sequence {b}: rel L2 {l2:.2e}, max element ratio {mr:.2e}")
 
 
 # (C % 4 != 0 takes the kernel's 4-byte-load path, the others its 16-byte one)

@@ -1,8 +1,8 @@
-"""Pins of the oracle's BMUF-NBM global step (§VI-B, eqs. (1)-(5)): special
+"""Pins of the oracle's BMUF-NBM global step (§VI-B, eqs. (2)-(6)): special
 cases that reduce to plain model averaging and to taking the single local
 model, a closed form of the block momentum over several blocks computed in
 exact rational arithmetic, the all-reduced-sum form of the average, and the
-hyper-parameter relation of eq. (5).  CPU only."""
+hyper-parameter relation of eq. (6).  CPU only."""
 
 from fractions import Fraction
 
@@ -32,7 +32,7 @@ def test_single_worker_without_momentum_takes_the_local_model():
 
 @pytest.mark.parametrize("workers", [2, 4, 8])
 def test_without_momentum_is_model_averaging(workers):
-    # eta = 0, zeta = 1: W_g(t) is the plain average of eq. (1), here exact
+    # eta = 0, zeta = 1: W_g(t) is the plain average of eq. (2), here exact
     rng = np.random.default_rng(workers)
     n = 300
     models = _grid(rng, (workers, n))
