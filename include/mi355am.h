@@ -182,6 +182,23 @@ am_status grad_threshold_encode(int64_t n, const float* grad, float* residual, f
                                 uint32_t* words, int64_t capacity, int64_t* count,
                                 void* ws, int64_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory or pass a workspace (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): grad_threshold_encode with the same kernels and results, its
+ * scratch held in a device array the library owns for the life of the
+ * process (each GPU that runs it holds its own copy of
+ * am_encode_workspace_bytes(AM_ENCODE_NOALLOC_MAX_N) = about 8.4 MB).  The
+ * first call on a GPU looks up that GPU's copy (no allocation); no call
+ * allocates or frees device memory.  n > AM_ENCODE_NOALLOC_MAX_N returns
+ * AM_EUNSUPPORTED with nothing enqueued; other arguments and errors as
+ * grad_threshold_encode.  Every call on one GPU shares that GPU's array:
+ * calls that may overlap on one GPU (different streams, or threads) race and
+ * must be ordered by the caller.  The array needs no clearing between calls. */
+#define AM_ENCODE_NOALLOC_MAX_N (1ll << 25) /* 33,554,432 elements */
+am_status grad_threshold_encode_noalloc(int64_t n, const float* grad, float* residual, float tau,
+                                        uint32_t* words, int64_t capacity, int64_t* count,
+                                        void* stream);
+
 /* Decode (§VI-A): dense[i] = +tau (sign bit 0) or -tau (sign bit 1) for each
  * of the first min(*count, capacity) words (count is a device int64, so no
  * host synchronisation is needed; capacity = number of words `words` holds);

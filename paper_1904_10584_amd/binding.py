@@ -73,6 +73,7 @@ _PROTOS = {
     "sparse_soft_ce": (_I32, [_I64, _I32, _I32, _P, _P, _P, _P, _I32, _P, _P, _I32, _P, _I64, _P]),
     "lstm_am_backward": (_I32, [_P, _P, _P, _P, _I32, _I32, _P, _P, _I64, _P, _P]),
     "grad_threshold_encode": (_I32, [_I64, _P, _P, _F32, _P, _I64, _P, _P, _I64, _P]),
+    "grad_threshold_encode_noalloc": (_I32, [_I64, _P, _P, _F32, _P, _I64, _P, _P]),
     "grad_threshold_decode": (_I32, [_P, _P, _I64, _F32, _I64, _P, _I32, _P]),
     "sgd_apply": (_I32, [_I64, _P, _P, _P, _F32, _P]),
     "am_decode_multi_workspace_bytes": (_I64, [_I32, _I64]),
@@ -236,6 +237,18 @@ def grad_threshold_encode(grad, residual, tau, words, count, ws, stream=None):
         float(tau), _dev(words, "words", torch.int32), words.numel(),
         _dev(count, "count", torch.int64), _dev(ws, "ws"), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+ENCODE_NOALLOC_MAX_N = 1 << 25
+
+
+def grad_threshold_encode_noalloc(grad, residual, tau, words, count, stream=None):
+    """grad_threshold_encode without a workspace (library-owned scratch)."""
+    n = grad.numel()
+    _check(lib().grad_threshold_encode_noalloc(
+        n, _dev(grad, "grad", torch.float32), _dev(residual, "residual", torch.float32),
+        float(tau), _dev(words, "words", torch.int32), words.numel(),
+        _dev(count, "count", torch.int64), _stream(stream)))
 
 
 def grad_threshold_decode(words, count, tau, dense, accumulate=False, stream=None):

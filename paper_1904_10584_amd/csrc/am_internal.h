@@ -145,7 +145,16 @@ struct SoftCeArgs {
 int64_t soft_ce_partials(int64_t N);
 hipError_t soft_ce(const SoftCeArgs& a, hipStream_t s);
 
-// Threshold encode / decode.
+// Threshold encode / decode.  The encoder's scratch: 2-bit codes (a 32-bit
+// word per 16 elements, TILE elements per tile) and one count per tile, each
+// region 256-byte aligned.
+constexpr int64_t GTC_TILE = 4096;
+constexpr int64_t gtc_tiles_c(int64_t n) { return (n + GTC_TILE - 1) / GTC_TILE; }
+constexpr int64_t gtc_align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+constexpr int64_t gtc_codes_bytes(int64_t n) { return gtc_align256(gtc_tiles_c(n) * (GTC_TILE / 4)); }
+constexpr int64_t gtc_encode_scratch_bytes(int64_t n) {
+  return gtc_codes_bytes(n) + gtc_align256(gtc_tiles_c(n) * 4);
+}
 int64_t gtc_tiles(int64_t n);
 hipError_t gtc_encode(int64_t n, const float* g, float* r, float tau, uint32_t* words,
                       int64_t* count, uint32_t* ws_mask, int32_t* ws_tile, hipStream_t s);

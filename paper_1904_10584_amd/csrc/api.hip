@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -457,6 +458,61 @@ TeacherWs teacher_ws_layout(const am_model* m, int64_t T, int64_t B, int64_t N) 
   return w;
 }
 
+// ------------------------------------------------- threshold encode --
+
+am_status check_encode_args(int64_t n, const float* grad, const float* residual, float tau,
+                            const uint32_t* words, int64_t capacity, const int64_t* count) {
+  if (n < 0 || n >= (1ll << 31)) return fail(AM_EINVAL, "n = %lld outside [0, 2^31)", (long long)n);
+  if (!(tau > 0.f)) return fail(AM_EINVAL, "tau must be > 0");
+  if (!count) return fail(AM_EINVAL, "count is NULL");
+  if (n > 0 && (!grad || !residual || !words)) return fail(AM_EINVAL, "NULL pointer");
+  if (capacity < n) return fail(AM_ECAPACITY, "capacity %lld < n %lld", (long long)capacity, (long long)n);
+  return AM_OK;
+}
+
+// The encode launches on a scratch area of gtc_encode_scratch_bytes(n)
+// (the codes, then the tile counts); every byte the kernels read there is
+// written by the same call first, so the area needs no clearing.
+am_status encode_with_scratch(int64_t n, const float* grad, float* residual, float tau,
+                              uint32_t* words, int64_t* count, void* scratch, hipStream_t s) {
+  uint32_t* codes = at<uint32_t>(scratch, 0);
+  int32_t* tile = at<int32_t>(scratch, am::gtc_codes_bytes(n));
+  Timed tm(AM_K_ENCODE, s, 0.0, 12.0 * n);
+  return hip_check(am::gtc_encode(n, grad, residual, tau, words, count, codes, tile, s), "encode");
+}
+
+// Scratch of grad_threshold_encode_noalloc: a device array owned by the
+// library for the life of the process (each GPU holds its own copy).  In
+// host code its name only stands in for the symbol; the device address of
+// a GPU's copy comes from hipGetSymbolAddress with that GPU current, once,
+// and is kept per device.
+constexpr int64_t NOALLOC_SCRATCH_BYTES = am::gtc_encode_scratch_bytes(AM_ENCODE_NOALLOC_MAX_N);
+static __device__ __align__(256) unsigned char encode_scratch[NOALLOC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+am_status encode_scratch_of(hipStream_t s, void** out) {
+  int cur = 0, dev = 0;
+  AM_TRY(hip_check(hipGetDevice(&cur), "hipGetDevice"));
+  dev = cur;
+  if (s) AM_TRY(hip_check(hipStreamGetDevice(s, &dev), "hipStreamGetDevice"));
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(AM_EUNSUPPORTED, "device %d >= %d", dev, MAX_DEVICES);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    if (dev != cur) AM_TRY(hip_check(hipSetDevice(dev), "hipSetDevice"));
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(encode_scratch));
+    if (dev != cur) AM_TRY(hip_check(hipSetDevice(cur), "hipSetDevice"));
+    AM_TRY(hip_check(e, "hipGetSymbolAddress(encode scratch)"));
+    if (!p || !aligned(p, 256)) return fail(AM_EHIP, "encode scratch has no 256-byte aligned address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return AM_OK;
+}
+
 }  // namespace
 
 // ================================================================= C ABI ==
@@ -520,8 +576,7 @@ int64_t am_ce_workspace_bytes(int64_t N) {
 
 int64_t am_encode_workspace_bytes(int64_t n) {
   if (n < 0) return -1;
-  const int64_t tiles = am::gtc_tiles(n);
-  return align256(tiles * 256 * 4) + align256(tiles * 4);
+  return am::gtc_encode_scratch_bytes(n);
 }
 
 am_status am_cast_f32_to_bf16(int64_t n, const float* src, void* dst, void* stream) {
@@ -545,20 +600,26 @@ am_status sgd_apply(int64_t n, float* master, void* weights_bf16, const float* u
 am_status grad_threshold_encode(int64_t n, const float* grad, float* residual, float tau,
                                 uint32_t* words, int64_t capacity, int64_t* count, void* ws,
                                 int64_t ws_bytes, void* stream) {
-  if (n < 0 || n >= (1ll << 31)) return fail(AM_EINVAL, "n = %lld outside [0, 2^31)", (long long)n);
-  if (!(tau > 0.f)) return fail(AM_EINVAL, "tau must be > 0");
-  if (!count) return fail(AM_EINVAL, "count is NULL");
-  if (n > 0 && (!grad || !residual || !words)) return fail(AM_EINVAL, "NULL pointer");
-  if (capacity < n) return fail(AM_ECAPACITY, "capacity %lld < n %lld", (long long)capacity, (long long)n);
+  AM_TRY(check_encode_args(n, grad, residual, tau, words, capacity, count));
   const int64_t need = am_encode_workspace_bytes(n);
   if (!ws || ws_bytes < need || !aligned(ws, 256))
     return fail(AM_EWORKSPACE, "encode needs %lld workspace bytes (256-aligned)", (long long)need);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int64_t tiles = am::gtc_tiles(n);
-  uint32_t* codes = at<uint32_t>(ws, 0);
-  int32_t* tile = at<int32_t>(ws, align256(tiles * 256 * 4));
-  Timed tm(AM_K_ENCODE, s, 0.0, 12.0 * n);
-  return hip_check(am::gtc_encode(n, grad, residual, tau, words, count, codes, tile, s), "encode");
+  return encode_with_scratch(n, grad, residual, tau, words, count, ws, s);
+}
+
+am_status grad_threshold_encode_noalloc(int64_t n, const float* grad, float* residual, float tau,
+                                        uint32_t* words, int64_t capacity, int64_t* count,
+                                        void* stream) {
+  AM_TRY(check_encode_args(n, grad, residual, tau, words, capacity, count));
+  if (n > AM_ENCODE_NOALLOC_MAX_N)
+    return fail(AM_EUNSUPPORTED, "grad_threshold_encode_noalloc handles n <= %lld (n = %lld); "
+                "use grad_threshold_encode with a workspace", (long long)AM_ENCODE_NOALLOC_MAX_N,
+                (long long)n);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* scratch = nullptr;
+  AM_TRY(encode_scratch_of(s, &scratch));
+  return encode_with_scratch(n, grad, residual, tau, words, count, scratch, s);
 }
 
 am_status grad_threshold_decode(const uint32_t* words, const int64_t* count, int64_t capacity,

@@ -21,7 +21,7 @@
 namespace am {
 namespace {
 
-constexpr int TILE = 4096;        // elements per tile
+constexpr int TILE = (int)GTC_TILE;  // elements per tile
 constexpr int TPB = 256;          // threads per block; 16 elements each
 // Element e of a tile is handled by thread (e % 1024) / 4 as item
 // (e / 1024) * 4 + e % 4: four float4 groups at stride 1024.
