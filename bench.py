@@ -20,6 +20,11 @@ import os
 import sys
 import time
 
+# The CPU oracle's BLAS threads: the cores this process may run on, unless
+# the environment already fixes the count (it is read when numpy loads).
+AFFINITY_CORES = len(os.sched_getaffinity(0))
+os.environ.setdefault("OMP_NUM_THREADS", str(AFFINITY_CORES))
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -42,6 +47,8 @@ def parse():
                          "target generation)")
     ap.add_argument("--cpu-chunks", type=int, default=0,
                     help="chunks the CPU oracle runs forward/backward on (0 = the whole batch)")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="skip the shorter measurement of the other workloads")
     return ap.parse_args()
 
 
@@ -53,14 +60,16 @@ def kernel_sources_digest(names):
     return h.hexdigest()[:16]
 
 
-def traffic_for(kclass, per_launch_units):
-    """HBM bytes per launch from a committed counter summary, if it still
-    matches the kernel sources (else None)."""
+def traffic_for(kclass, per_launch_units, workload="paper-5x768"):
+    """HBM bytes per launch from a committed counter summary of this
+    workload, if it still matches the kernel sources (else None)."""
     path = os.path.join(ROOT, "profiles", "counters.json")
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         table = json.load(fh)
+    if table.get("workload", "paper-5x768") != workload:
+        return None
     ent = table.get(kclass)
     if not ent:
         return None
@@ -350,17 +359,86 @@ def teacher_kernels(am, synth, w, reps):
     return out
 
 
+def blas_threads():
+    """Threads the oracle's BLAS actually runs with."""
+    try:
+        from threadpoolctl import threadpool_info
+        return int(max((i.get("num_threads", 1) for i in threadpool_info()), default=1))
+    except Exception:
+        return 1
+
+
+def cpu_oracle_step(wl, synth, S, seq_lengths=None):
+    """The oracle's forward + CE + BPTT on S sequences of workload `wl` (all
+    of T frames, or the given lengths); returns (seconds, frames)."""
+    import numpy as np
+    import oracle
+    w = synth.WORKLOADS[wl]
+    d = oracle.ModelDims(w["layers"], w["input_dim"], w["hidden"], w["classes"])
+    n = oracle.param_count(d)
+    master = synth.init_params(n, d.hidden)
+    T = w["T"] if seq_lengths is None else int(seq_lengths[0])
+    counts, offs = oracle.batch_schedule(T, S, seq_lengths)
+    N = int(offs[-1])
+    x = synth.features(N, d.input_dim)
+    idx, prob = synth.teacher_targets(N, d.classes, w["K"], w["mass"],
+                                      one_hot_frac=w.get("one_hot_frac", 0.0))
+    bf = w["dtype"] == "bf16"
+    p = oracle.bf16_round(master) if bf else master
+    xe = oracle.bf16_round(x) if bf else x
+    t0 = time.perf_counter()
+    logits, cache = oracle.lstm_am_forward(p, d, xe, T, S, seq_lengths)
+    loss, dz = oracle.sparse_soft_ce(logits, idx, prob)
+    oracle.lstm_am_backward(p, d, cache, dz)
+    return time.perf_counter() - t0, N
+
+
+def cpu_baseline_other(synth):
+    """The oracle on bounded samples of the other workloads: frames/s of the
+    forward + CE + BPTT (the per-frame cost of these loops does not depend on
+    the batch), and the quantiser of the 24,145,848-parameter model over 10
+    consecutive steps with residual feedback (5 of them timed)."""
+    import numpy as np
+    import oracle
+    out = {}
+    for wl, S, lens in (("tiny-2x64", 16, None), ("wide-5x1536", 32, None),
+                        ("varlen-5x768", 4, None)):
+        if wl == "varlen-5x768":  # utterances spread over the sorted lengths
+            w = synth.WORKLOADS[wl]
+            all_lens = synth.utterance_lengths(w["B"], w["len_lo"], w["len_hi"])
+            lens = all_lens[[0, 43, 86, 127]].astype(np.int32)
+        sec, frames = cpu_oracle_step(wl, synth, S, lens)
+        out[wl] = {"value": round(frames / sec, 2), "unit": "frames/s", "cores": blas_threads(),
+                   "kind": "oracle",
+                   "sample": f"forward+CE+BPTT of {S} sequences ({frames} frames, {sec:.1f} s)"}
+    w = synth.WORKLOADS["paper-5x768"]
+    n = oracle.param_count(oracle.ModelDims(w["layers"], w["input_dim"], w["hidden"], w["classes"]))
+    rng = np.random.default_rng(9)
+    tau = np.float32(w["tau"])
+    r = np.zeros(n, np.float32)
+    master = synth.init_params(n, w["hidden"])
+    g = (rng.standard_normal(n) * 3e-5).astype(np.float32)
+    steps, t0 = 5, time.perf_counter()
+    for _ in range(steps):
+        r, words, count = oracle.grad_threshold_encode(g, r, tau)
+        u = oracle.grad_threshold_decode(words, count, tau, n)
+        master, _ = oracle.sgd_apply(master, u, w["lr"])
+    sec = (time.perf_counter() - t0) / steps
+    out["gtc-100-steps"] = {"value": round(1e3 * sec, 1), "unit": "ms per quantiser step",
+                            "cores": 1, "kind": "oracle",
+                            "sample": (f"encode + decode + SGD of all {n} parameters, 5 of the "
+                                       f"100 consecutive steps (N(0, 3e-5^2) gradients, "
+                                       f"tau = 1e-4), {sec:.2f} s per step")}
+    return out
+
+
 def cpu_baseline(wl, synth, chunks):
     """The oracle, as it stands, on a bounded sample: forward, CE and BPTT on
     `chunks` chunks of the batch, plus encode, decode and SGD of the whole
     flat gradient; scaled to frames/s of a full step."""
     import numpy as np
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
-    except Exception:
-        threads = 1
+    threads = blas_threads()
     w = synth.WORKLOADS[wl]
     d = oracle.ModelDims(w["layers"], w["input_dim"], w["hidden"], w["classes"])
     n = oracle.param_count(d)
@@ -382,10 +460,73 @@ def cpu_baseline(wl, synth, chunks):
     t2 = time.perf_counter()
     step_s = (t1 - t0) * (B / S) + (t2 - t1)
     return {"value": round(T * B / step_s, 2), "unit": "frames/s", "cores": int(threads),
-            "kind": "oracle",
+            "affinity_cores": AFFINITY_CORES, "kind": "oracle",
             "sample": (f"fp64 numpy oracle: forward+CE+BPTT on {S} of {B} chunks x {T} frames "
                        f"({t1 - t0:.1f} s, scaled x{B / S:g}) plus encode/decode/SGD of all "
                        f"{n} parameters ({t2 - t1:.1f} s)")}
+
+
+def measure(wl, steps, warmup, am, synth, trainer):
+    """One workload: warm-up steps, one recorded step with every kernel class
+    (to find the class that takes the most time), then `steps` timed steps
+    with that class bracketed by HIP events on its stream.  Returns the step
+    time, frames/s, MFMA utilisation over the step, the roofline of the
+    dominant class and the per-class milliseconds of the recorded step."""
+    import torch
+    st, w, T, lengths = make_step(wl, am, synth, trainer)
+    for _ in range(warmup):
+        st.step()
+    torch.cuda.synchronize()
+    classes = range(len(am.KERNEL_CLASSES))
+    am.profile_begin(classes)
+    st.step()
+    am.profile_end()
+    totals = {k: am.profile_get(k) for k in classes}
+    dom = max(classes, key=lambda k: totals[k]["ms"])
+    torch.cuda.synchronize()
+
+    am.profile_begin([dom])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        st.step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    am.profile_end()
+    st.check()  # a timed-out step barrier invalidates the measurement
+    kt = am.profile_get(dom)
+    ms_per_step = (t1 - t0) * 1e3 / steps
+    flops, N = step_flops(w, T, lengths)
+    frames_per_s = N / (ms_per_step * 1e-3)
+
+    avg_ms = kt["ms"] / max(kt["launches"], 1)
+    name = am.KERNEL_CLASSES[dom]
+    hbm_classes = {am.K_CE, am.K_ENCODE, am.K_DECODE, am.K_SGD, am.K_MISC}
+    bf16 = w["dtype"] == "bf16"
+    peak_mfma = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+    if dom in hbm_classes:
+        per_launch = kt["bytes"] / max(kt["launches"], 1)
+        achieved = per_launch / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    else:
+        per_launch = kt["flops"] / max(kt["launches"], 1)
+        achieved = per_launch / (avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak_mfma, "unit": "TFLOP/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = traffic_for(name, per_launch, wl)
+    roof["kernel"] = name
+    roof["launches_per_step"] = kt["launches"] // steps
+    roof["avg_launch_us"] = round(avg_ms * 1e3, 2)
+    roof["algorithmic_per_launch"] = per_launch
+    res = {
+        "st": st, "w": w, "T": T, "lengths": lengths, "N": N, "flops": flops, "bf16": bf16,
+        "ms_per_step": ms_per_step, "frames_per_s": frames_per_s,
+        "mfma_util_pct": round(100.0 * flops / (ms_per_step * 1e-3) / (peak_mfma * 1e12), 2),
+        "roofline": roof,
+        "kernel_ms_per_step": {am.KERNEL_CLASSES[k]: round(totals[k]["ms"], 3) for k in classes
+                               if totals[k]["launches"] > 0},
+    }
+    return res
 
 
 def main():
@@ -399,68 +540,22 @@ def main():
     from paper_1904_10584_amd import synth, trainer
 
     torch.cuda.set_device(0)
-    st, w, T, lengths = make_step(args.workload, am, synth, trainer)
-
-    # warm-up, then one recorded step with every kernel class to find the
-    # class that takes the most time
-    for _ in range(args.warmup):
-        st.step()
-    torch.cuda.synchronize()
-    classes = range(len(am.KERNEL_CLASSES))
-    am.profile_begin(classes)
-    st.step()
-    am.profile_end()
-    totals = {k: am.profile_get(k) for k in classes}
-    dom = max(classes, key=lambda k: totals[k]["ms"])
-    torch.cuda.synchronize()
-
-    # timed steps; the dominant class is bracketed by HIP events on its stream
-    am.profile_begin([dom])
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        st.step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    am.profile_end()
-    st.check()  # a timed-out step barrier invalidates the measurement
-    kt = am.profile_get(dom)
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    flops, N = step_flops(w, T, lengths)
-    frames_per_s = N / (ms_per_step * 1e-3)
-
-    avg_ms = kt["ms"] / max(kt["launches"], 1)
-    name = am.KERNEL_CLASSES[dom]
-    hbm_classes = {am.K_CE, am.K_ENCODE, am.K_DECODE, am.K_SGD, am.K_MISC}
-    bf16 = w["dtype"] == "bf16"
-    if dom in hbm_classes:
-        per_launch = kt["bytes"] / max(kt["launches"], 1)
-        achieved = per_launch / (avg_ms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
-    else:
-        per_launch = kt["flops"] / max(kt["launches"], 1)
-        achieved = per_launch / (avg_ms * 1e-3) / 1e12
-        peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s"}
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = traffic_for(name, per_launch)
-    roof["kernel"] = name
-    roof["launches_per_step"] = kt["launches"] // args.steps
-    roof["avg_launch_us"] = round(avg_ms * 1e3, 2)
-    roof["algorithmic_per_launch"] = per_launch
-
+    r = measure(args.workload, args.steps, args.warmup, am, synth, trainer)
+    w, T, lengths, N = r["w"], r["T"], r["lengths"], r["N"]
+    n = r["st"].n
+    del r["st"]
     out = {
         "metric": METRIC,
-        "value": round(frames_per_s, 1),
+        "value": round(r["frames_per_s"], 1),
         "unit": "frames/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 3),
+        "ms_per_step": round(r["ms_per_step"], 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if bf16 else "f32",
+        "dtype": "bf16" if r["bf16"] else "f32",
         "data": "synthetic",
         "config": {"workload": args.workload, "layers": w["layers"], "hidden": w["hidden"],
                    "input_dim": w["input_dim"], "classes": w["classes"], "chunks": w["B"],
@@ -468,22 +563,37 @@ def main():
                    "frames_per_step": N, "k": w["K"], "tau": w["tau"], "lr": w["lr"],
                    "step": "forward+soft_ce+bptt+threshold_encode+decode+sgd",
                    "parallelism": "single-gpu"},
-        "mfma_util_pct": round(100.0 * flops / (ms_per_step * 1e-3) / (
-            (PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS) * 1e12), 2),
-        "step_tflop": round(flops / 1e12, 4),
-        "roofline": roof,
-        "kernel_ms_per_step": {am.KERNEL_CLASSES[k]: round(totals[k]["ms"], 3) for k in classes
-                               if totals[k]["launches"] > 0},
+        "mfma_util_pct": r["mfma_util_pct"],
+        "step_tflop": round(r["flops"] / 1e12, 4),
+        "roofline": r["roofline"],
+        "kernel_ms_per_step": r["kernel_ms_per_step"],
     }
+    torch.cuda.empty_cache()
+    if not args.no_other_workloads and args.workload == "paper-5x768":
+        # the other training workloads, fewer steps each (their own roofline
+        # and per-class times)
+        other = {}
+        for wl, steps in (("wide-5x1536", 10), ("varlen-5x768", 10)):
+            o = measure(wl, steps, 2, am, synth, trainer)
+            del o["st"]
+            other[wl] = {"value": round(o["frames_per_s"], 1), "unit": "frames/s",
+                         "ms_per_step": round(o["ms_per_step"], 3), "steps": steps, "warmup": 2,
+                         "frames_per_step": o["N"], "step_tflop": round(o["flops"] / 1e12, 4),
+                         "mfma_util_pct": o["mfma_util_pct"], "roofline": o["roofline"],
+                         "kernel_ms_per_step": o["kernel_ms_per_step"]}
+            torch.cuda.empty_cache()
+        out["other_workloads"] = other
     if not args.no_worker_kernels:
-        out["hbm_kernels"] = hbm_kernels(am, synth, w, st.n, reps=10)
-        out["worker_kernels"] = worker_kernels(am, st.n, reps=10)
+        out["hbm_kernels"] = hbm_kernels(am, synth, w, n, reps=10)
+        out["worker_kernels"] = worker_kernels(am, n, reps=10)
         if lengths is None:
             out["input_kernels"] = input_kernels(am, synth, w, N, reps=10)
-            if bf16:
+            if r["bf16"]:
                 out["teacher_kernels"] = teacher_kernels(am, synth, w, reps=5)
     if not args.no_cpu_baseline and args.workload in ("paper-5x768", "tiny-2x64", "wide-5x1536"):
         out["cpu_baseline"] = cpu_baseline(args.workload, synth, args.cpu_chunks)
+        if args.workload == "paper-5x768":
+            out["cpu_baseline_other"] = cpu_baseline_other(synth)
     print(json.dumps(out), flush=True)
 
 
