@@ -518,7 +518,19 @@ def measure(wl, steps, warmup, am, synth, trainer):
     roof["launches_per_step"] = kt["launches"] // steps
     roof["avg_launch_us"] = round(avg_ms * 1e3, 2)
     roof["algorithmic_per_launch"] = per_launch
+    # the quantiser at the step's own send rate (the recorded step's encode:
+    # 12 B per element + 4 B per emitted word)
+    count = int(st.count.item())
+    ke = totals[am.K_ENCODE]
+    enc = None
+    if ke["launches"] > 0 and ke["ms"] > 0:
+        ebytes = 12.0 * st.n + 4.0 * count
+        egbs = ebytes / (ke["ms"] * 1e-3) / 1e9
+        enc = {"send_rate": round(count / st.n, 5), "us": round(ke["ms"] * 1e3, 2),
+               "algorithmic_bytes": ebytes, "achieved_GBs": round(egbs, 1),
+               "frac": round(egbs / PEAK_HBM_GBS, 4)}
     res = {
+        "encode_at_step_rate": enc,
         "st": st, "w": w, "T": T, "lengths": lengths, "N": N, "flops": flops, "bf16": bf16,
         "ms_per_step": ms_per_step, "frames_per_s": frames_per_s,
         "mfma_util_pct": round(100.0 * flops / (ms_per_step * 1e-3) / (peak_mfma * 1e12), 2),
@@ -567,6 +579,7 @@ def main():
         "step_tflop": round(r["flops"] / 1e12, 4),
         "roofline": r["roofline"],
         "kernel_ms_per_step": r["kernel_ms_per_step"],
+        "encode_at_step_rate": r["encode_at_step_rate"],
     }
     torch.cuda.empty_cache()
     if not args.no_other_workloads and args.workload == "paper-5x768":

@@ -475,9 +475,9 @@ am_status check_encode_args(int64_t n, const float* grad, const float* residual,
 // written by the same call first, so the area needs no clearing.
 am_status encode_with_scratch(int64_t n, const float* grad, float* residual, float tau,
                               uint32_t* words, int64_t* count, void* scratch, hipStream_t s) {
+  Timed tm(AM_K_ENCODE, s, 0.0, 12.0 * n);
   uint32_t* codes = at<uint32_t>(scratch, 0);
   int32_t* tile = at<int32_t>(scratch, am::gtc_codes_bytes(n));
-  Timed tm(AM_K_ENCODE, s, 0.0, 12.0 * n);
   return hip_check(am::gtc_encode(n, grad, residual, tau, words, count, codes, tile, s), "encode");
 }
 

@@ -3,13 +3,17 @@
 // and the matching decode.  Exact fp32 (single adds/subtracts, IEEE
 // subnormals), so the result is bit-identical to the element-wise definition.
 //
-// Encode runs in three HBM-bound passes over tiles of 4096 elements:
+// Encode runs in two launches over tiles of 4096 elements:
 //   1. update: a = r + g; r <- a -+ tau where |a| > tau; a 2-bit code per
 //      element (sent, sign) is packed 16 codes per thread word; per-tile count.
 //      Reads g and r, writes r: 12 bytes per element plus 1/4 byte of codes.
-//   2. scan: exclusive prefix over the tile counts (one block) and the total.
-//   3. compact: each tile re-reads its 1 KB of codes, ranks the sent elements
-//      in index order and writes their words contiguously.
+//   2. compact: each tile's block sums the counts of the tiles before it
+//      (up to 8192 tiles; beyond, a one-block scan turns the counts into
+//      offsets first), ranks its sent elements in index order into LDS and
+//      writes their words contiguously.
+// Measured alternatives (a single resident launch with the codes kept on
+// chip, super-tile counts by atomics, a fused scan) streamed the update
+// slower or serialised on atomics.
 // Decode builds each 4096-element tile of the dense update in LDS (zero or
 // the existing values, then +-tau at the indices of the tile's words, found
 // by binary search in the ascending word list) and writes it once.  The
@@ -103,22 +107,21 @@ __global__ __launch_bounds__(1024) void gtc_scan(int32_t* __restrict__ tile_coun
   if (t == 1023) *total = part[1023];
 }
 
-__global__ __launch_bounds__(TPB) void gtc_compact(int64_t n, const uint32_t* __restrict__ codes,
-                                                   const int32_t* __restrict__ tile_off,
-                                                   uint32_t* __restrict__ words) {
-  __shared__ uint64_t wtot[TPB / 64];
+// Ranks of one tile's sent elements, in index order: thread t's code word
+// covers elements 1024 grp + 4 t + c of the tile (grp, c < 4), so per group
+// the 16-bit field counts are scanned over the threads.  Each word goes to
+// its place in the tile's LDS buffer; returns the tile's word count.
+__device__ __forceinline__ uint32_t rank_tile(uint32_t code, uint32_t tile_base, uint32_t* buf,
+                                              uint64_t* wtot) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint32_t code = codes[(int64_t)blockIdx.x * TPB + threadIdx.x];
-  // per-group counts packed in 16-bit fields: field grp = sent items of group grp
   uint64_t mine = 0;
 #pragma unroll
   for (int grp = 0; grp < 4; ++grp)
     mine |= (uint64_t)__popc((code >> (8 * grp)) & 0x55u) << (16 * grp);
-  // inclusive wave scan
   uint64_t inc = mine;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    uint64_t v = __shfl_up(inc, o, 64);
+    const uint64_t v = __shfl_up(inc, o, 64);
     if (lane >= o) inc += v;
   }
   if (lane == 63) wtot[wave] = inc;
@@ -129,22 +132,79 @@ __global__ __launch_bounds__(TPB) void gtc_compact(int64_t n, const uint32_t* __
     if (w < wave) before += wtot[w];
     total += wtot[w];
   }
-  const uint64_t excl = before + inc - mine;  // sent items in earlier threads, per group
-  int64_t pos = tile_off[blockIdx.x];
-  const int64_t base = (int64_t)blockIdx.x * TILE;
+  const uint64_t excl = before + inc - mine;
+  const uint32_t e0 = tile_base + threadIdx.x * 4;
+  uint32_t lp = 0;
 #pragma unroll
   for (int grp = 0; grp < 4; ++grp) {
-    int64_t p = pos + (int64_t)((excl >> (16 * grp)) & 0xFFFFu);
+    uint32_t p = lp + (uint32_t)((excl >> (16 * grp)) & 0xFFFFu);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const uint32_t k = (code >> (2 * (grp * 4 + c))) & 3u;
-      if (k & 1u) {
-        const uint32_t e = (uint32_t)(base + grp * 1024 + threadIdx.x * 4 + c);
-        words[p++] = (e << 1) | (k >> 1);
+      if (k & 1u) buf[p++] = ((e0 + grp * 1024 + c) << 1) | (k >> 1);
+    }
+    lp += (uint32_t)((total >> (16 * grp)) & 0xFFFFu);
+  }
+  __syncthreads();
+  return lp;
+}
+
+// Compaction for up to OWN_PREFIX_TILES tiles: each block sums the counts of
+// every earlier tile itself (16-byte loads, all issued at once; they hit the
+// L2), so no scan launch sits between the update and the compaction.  The
+// tile's words are ranked into LDS and leave as consecutive 4-byte stores.
+// The last tile's block writes the total.
+constexpr int64_t OWN_PREFIX_TILES = 8 * TPB * 4;  // 8192 tiles: n <= 2^25
+
+__global__ __launch_bounds__(TPB) void gtc_compact_own_prefix(int64_t ntiles,
+                                                              const uint32_t* __restrict__ codes,
+                                                              const int32_t* __restrict__ tile_count,
+                                                              uint32_t* __restrict__ words,
+                                                              int64_t* __restrict__ total_out) {
+  __shared__ uint32_t buf[TILE];
+  __shared__ uint64_t wtot[TPB / 64];
+  __shared__ uint32_t wpre[TPB / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t t = blockIdx.x;
+  const uint32_t code = codes[t * TPB + threadIdx.x];
+  uint32_t pre = 0;
+  {
+    int4 q[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int64_t j = ((int64_t)i * TPB + threadIdx.x) * 4;
+      if (j + 3 < t) {
+        q[i] = *reinterpret_cast<const int4*>(tile_count + j);
+      } else {
+        q[i].x = j < t ? tile_count[j] : 0;
+        q[i].y = j + 1 < t ? tile_count[j + 1] : 0;
+        q[i].z = j + 2 < t ? tile_count[j + 2] : 0;
+        q[i].w = 0;
       }
     }
-    pos += (int64_t)((total >> (16 * grp)) & 0xFFFFu);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pre += (uint32_t)((q[i].x + q[i].y) + (q[i].z + q[i].w));
   }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) pre += __shfl_xor(pre, o, 64);
+  if (lane == 0) wpre[wave] = pre;
+  const uint32_t lp = rank_tile(code, (uint32_t)(t * TILE), buf, wtot);  // (its barrier orders wpre)
+  const uint32_t pos = ((wpre[0] + wpre[1]) + wpre[2]) + wpre[3];
+  for (uint32_t i = threadIdx.x; i < lp; i += TPB) words[pos + i] = buf[i];
+  if (t == ntiles - 1 && threadIdx.x == 0) *total_out = (int64_t)pos + lp;
+}
+
+// Compaction after a scan of the tile counts into offsets (more tiles).
+__global__ __launch_bounds__(TPB) void gtc_compact(const uint32_t* __restrict__ codes,
+                                                   const int32_t* __restrict__ tile_off,
+                                                   uint32_t* __restrict__ words) {
+  __shared__ uint32_t buf[TILE];
+  __shared__ uint64_t wtot[TPB / 64];
+  const int64_t t = blockIdx.x;
+  const uint32_t code = codes[t * TPB + threadIdx.x];
+  const uint32_t pos = (uint32_t)tile_off[t];
+  const uint32_t lp = rank_tile(code, (uint32_t)(t * TILE), buf, wtot);
+  for (uint32_t i = threadIdx.x; i < lp; i += TPB) words[pos + i] = buf[i];
 }
 
 __device__ __forceinline__ int64_t lower_bound_words(const uint32_t* w, int64_t cnt, uint32_t key) {
@@ -293,10 +353,14 @@ hipError_t gtc_encode(int64_t n, const float* g, float* r, float tau, uint32_t* 
       hipLaunchKernelGGL(gtc_update<false>, dim3((unsigned)ntiles), dim3(TPB), 0, s, n, g, r, tau,
                          ws_codes, ws_tile);
   }
+  if (ntiles > 0 && ntiles <= OWN_PREFIX_TILES) {
+    hipLaunchKernelGGL(gtc_compact_own_prefix, dim3((unsigned)ntiles), dim3(TPB), 0, s, ntiles,
+                       ws_codes, ws_tile, words, count);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(gtc_scan, dim3(1), dim3(1024), 0, s, ws_tile, ntiles, count);
   if (ntiles > 0)
-    hipLaunchKernelGGL(gtc_compact, dim3((unsigned)ntiles), dim3(TPB), 0, s, n, ws_codes, ws_tile,
-                       words);
+    hipLaunchKernelGGL(gtc_compact, dim3((unsigned)ntiles), dim3(TPB), 0, s, ws_codes, ws_tile, words);
   return hipGetLastError();
 }
 

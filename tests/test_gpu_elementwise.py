@@ -57,7 +57,9 @@ def _encode_gpu(g, r, tau, capacity=None):
     return rd.cpu().numpy(), words.cpu().numpy().view(np.uint32)[:c], c, words, count
 
 
-@pytest.mark.parametrize("n", [0, 1, 4095, 4096, 4097, 1_000_003])
+# (beyond 8192 tiles of 4096 elements the compaction takes a scan of the
+# tile counts: 40,000,003)
+@pytest.mark.parametrize("n", [0, 1, 4095, 4096, 4097, 1_000_003, 40_000_003])
 def test_encode_bit_exact(n):
     say(f"encode n={n}")
     rng = np.random.default_rng(n + 1)
@@ -111,6 +113,27 @@ def test_encode_multi_step_residual_feedback():
         assert c == ref_c, step
         np.testing.assert_array_equal(_bits32(rd.cpu().numpy()), _bits32(r))
         np.testing.assert_array_equal(words.cpu().numpy().view(np.uint32)[:c], ref_w)
+
+
+def test_encode_workspace_reused_across_sizes():
+    # one workspace serves calls of different sizes in any order: what a
+    # larger call leaves in the scratch never reaches a smaller one
+    rng = np.random.default_rng(17)
+    tau = np.float32(1e-4)
+    nmax = 24_145_848
+    ws = torch.zeros(am.encode_workspace_bytes(nmax), dtype=torch.uint8, device="cuda")
+    words = torch.zeros(nmax, dtype=torch.int32, device="cuda")
+    count = torch.zeros(1, dtype=torch.int64, device="cuda")
+    for n in (1_000_003, 5_000, nmax, 40_000, 1_000_003):
+        g = (rng.standard_normal(n) * 1e-4).astype(np.float32)
+        r = (rng.standard_normal(n) * 5e-5).astype(np.float32)
+        ref_r, ref_w, ref_c = oracle.grad_threshold_encode(g, r, tau)
+        rd = to_dev(r)
+        am.grad_threshold_encode(to_dev(g), rd, tau, words[:n], count, ws)
+        c = int(count.cpu()[0])
+        assert c == ref_c, n
+        np.testing.assert_array_equal(_bits32(rd.cpu().numpy()), _bits32(ref_r))
+        np.testing.assert_array_equal(words[:c].cpu().numpy().view(np.uint32), ref_w)
 
 
 @pytest.mark.parametrize("accumulate", [False, True])

@@ -27,7 +27,7 @@ def _encode(n, seed, tau, noalloc):
     if noalloc:
         am.grad_threshold_encode_noalloc(g, r, tau, words, count)
     else:
-        ws = torch.empty(am.encode_workspace_bytes(n), dtype=torch.uint8, device="cuda")
+        ws = torch.zeros(am.encode_workspace_bytes(n), dtype=torch.uint8, device="cuda")
         am.grad_threshold_encode(g, r, tau, words, count, ws)
     torch.cuda.synchronize()
     c = int(count.cpu()[0])
