@@ -32,6 +32,10 @@ struct GemmArgs {
 hipError_t gemm(const GemmArgs& g, hipStream_t s);
 // The bf16 products (gemm routes bf16 arguments here).
 hipError_t gemm_bf16(const GemmArgs& g, hipStream_t s);
+// A k-major, B n-major, K split up to max_splits ways: fp32 partials
+// part[S][M][N] (S returned in *splits), summed by the consumer in split order.
+hipError_t gemm_bf16_splitk_rows(const GemmArgs& g, int max_splits, float* part, int* splits,
+                                 hipStream_t s);
 // Sum of S split-K partial results [S][M][N] (and partial row sums [S][M])
 // into g.C / g.C2 (and g.rowsum), in split order.
 hipError_t splitk_reduce_launch(const float* part, int S, const GemmArgs& g, const float* rs_part,
@@ -70,6 +74,13 @@ struct LstmBwdStep {
   bool bf16;
 };
 hipError_t lstm_bwd_step(const LstmBwdStep& a, hipStream_t s);
+// bf16 steps as a batched product plus a cell kernel: the cell of a forward
+// step from pre = h_{t-1} Wh^T ([nb][4H] fp32, or null for a zero h_{t-1});
+// the cell backward from dhrec = dA_{t+1} Wh (`splits` partials
+// [splits][nbn][H] fp32, summed in order).  The product's
+// operands of `a` (Wh, WhT, dAnext) are not read here.
+hipError_t lstm_cell_fwd(const float* pre, const LstmFwdStep& a, hipStream_t s);
+hipError_t lstm_cell_bwd(const float* dhrec, int splits, const LstmBwdStep& a, hipStream_t s);
 
 // Persistent layer kernels (all time steps in one launch of a resident grid).
 // The schedule of a batch: T steps, B sequences, N frames; with varlen the

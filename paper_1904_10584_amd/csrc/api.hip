@@ -247,7 +247,7 @@ am::PersistSchedule persist_schedule(const Schedule& sc) {
 // Workspace carve-up (256-byte aligned regions).
 struct WsLayout {
   std::vector<int64_t> h, hs, c, g;  // per layer
-  int64_t p_da, dh, wht, dc, c0, h0, splitk, splitk_floats, sync, total;
+  int64_t p_da, dh, wht, dc, c0, h0, pre, splitk, splitk_floats, sync, total;
   static constexpr int MAX_SPLITS = 8;
 };
 
@@ -273,6 +273,7 @@ WsLayout ws_layout(const am_model* m, int64_t B, int64_t N) {
   w.dc = take(B * H * 4);
   w.c0 = take(L * B * H * 4);
   w.h0 = take(L * B * H * e);
+  w.pre = take(B * G * 4);  // one step's recurrent product (per-step path)
   // split-K partials of the weight-gradient products (plus partial row sums)
   const int64_t D0 = m->input_dim;
   const int64_t wide = (D0 > H ? D0 : H) + H;
@@ -282,6 +283,31 @@ WsLayout ws_layout(const am_model* m, int64_t B, int64_t N) {
   w.splitk = take(w.splitk_floats * 4);
   w.total = pos;
   return w;
+}
+
+template <typename P> P* at(void* base, int64_t off) {
+  return reinterpret_cast<P*>(static_cast<char*>(base) + off);
+}
+
+double gemm_bytes(int64_t M, int64_t N, int64_t K, int64_t e, int64_t out) {
+  return (double)(M * K + N * K) * e + (double)(M * N) * out;
+}
+
+am_status run_gemm(int cls, const am::GemmArgs& g, hipStream_t s) {
+  const int64_t e = g.bf16 ? 2 : 4;
+  Timed tm(cls, s, 2.0 * g.M * g.N * (double)g.K, gemm_bytes(g.M, g.N, g.K, e, g.c_f32 ? 4 : e));
+  return hip_check(am::gemm(g, s), "gemm");
+}
+
+am::GemmArgs mk_gemm(const void* A, int64_t lda, bool ak, const void* B, int64_t ldb, bool bk,
+                     void* C, int64_t ldc, bool cf32, const void* bias, int M, int N, int K,
+                     bool bf16) {
+  am::GemmArgs g;
+  g.A = A; g.lda = lda; g.a_kmajor = ak;
+  g.B = B; g.ldb = ldb; g.b_kmajor = bk;
+  g.C = C; g.ldc = ldc; g.c_f32 = cf32;
+  g.bias = bias; g.M = M; g.N = N; g.K = K; g.bf16 = bf16;
+  return g;
 }
 
 // One layer's recurrence, forward in time, over the packed rows of a
@@ -295,6 +321,7 @@ struct FwdLayer {
   void* H; void* Hs; float* C; void* G;  // outputs [N][H], [N][H], [N][H], [N][4H]
   void* sync;         // this launch's slot of the workspace's sync area (cleared)
   int* err;           // the time-out flag
+  float* pre;         // [B][4H] fp32 scratch of the per-step path
 };
 
 am_status forward_recurrence(const FwdLayer& f, const Schedule& sc, bool bf, int64_t H,
@@ -354,37 +381,26 @@ am_status forward_recurrence(const FwdLayer& f, const Schedule& sc, bool bf, int
     a.nb = (int)nb;
     a.hidden = (int)H;
     a.bf16 = bf;
+    if (bf) {
+      // the step's recurrent product as a batched product (few rows: square
+      // tiles that fill the CUs), then the cell
+      float* pre = nullptr;
+      if (a.hprev) {
+        AM_TRY(run_gemm(AM_K_LSTM_FWD,
+                        mk_gemm(a.hprev, H, true, f.Wh, H, true, f.pre, G, true, nullptr, (int)nb,
+                                (int)G, (int)H, true), s));
+        pre = f.pre;
+      }
+      Timed tm(AM_K_LSTM_FWD, s, 0.0, (double)nb * (G * (4.0 + e) + H * (2 * e + 8) + G * e));
+      AM_TRY(hip_check(am::lstm_cell_fwd(pre, a, s), "lstm forward cell"));
+      continue;
+    }
     const double bytes = (double)(nb * H + G * H + nb * G) * e + nb * H * 4.0 +
                          (double)nb * (H * (2 * e + 4) + G * e);
     Timed tm(AM_K_LSTM_FWD, s, 2.0 * nb * G * H, bytes);
     AM_TRY(hip_check(am::lstm_fwd_step(a, s), "lstm forward step"));
   }
   return AM_OK;
-}
-
-template <typename P> P* at(void* base, int64_t off) {
-  return reinterpret_cast<P*>(static_cast<char*>(base) + off);
-}
-
-double gemm_bytes(int64_t M, int64_t N, int64_t K, int64_t e, int64_t out) {
-  return (double)(M * K + N * K) * e + (double)(M * N) * out;
-}
-
-am_status run_gemm(int cls, const am::GemmArgs& g, hipStream_t s) {
-  const int64_t e = g.bf16 ? 2 : 4;
-  Timed tm(cls, s, 2.0 * g.M * g.N * (double)g.K, gemm_bytes(g.M, g.N, g.K, e, g.c_f32 ? 4 : e));
-  return hip_check(am::gemm(g, s), "gemm");
-}
-
-am::GemmArgs mk_gemm(const void* A, int64_t lda, bool ak, const void* B, int64_t ldb, bool bk,
-                     void* C, int64_t ldc, bool cf32, const void* bias, int M, int N, int K,
-                     bool bf16) {
-  am::GemmArgs g;
-  g.A = A; g.lda = lda; g.a_kmajor = ak;
-  g.B = B; g.ldb = ldb; g.b_kmajor = bk;
-  g.C = C; g.ldc = ldc; g.c_f32 = cf32;
-  g.bias = bias; g.M = M; g.N = N; g.K = K; g.bf16 = bf16;
-  return g;
 }
 
 // Weight gradient  [C | C2] = A^T [B | B2]  (K = frames), fp32, with the
@@ -433,7 +449,7 @@ TeacherOffsets teacher_layout(const am_model* m) {
 }
 
 struct TeacherWs {
-  int64_t sync, offs, lens, cat0, cat1, rev, p, hdir, hs, c, g, c0, total;
+  int64_t sync, offs, lens, cat0, cat1, rev, p, hdir, hs, c, g, c0, pre, total;
 };
 
 TeacherWs teacher_ws_layout(const am_model* m, int64_t T, int64_t B, int64_t N) {
@@ -454,6 +470,7 @@ TeacherWs teacher_ws_layout(const am_model* m, int64_t T, int64_t B, int64_t N) 
   w.c = take(N * H * 4);
   w.g = take(N * G * e);
   w.c0 = take(B * H * 4);
+  w.pre = take(B * G * 4);
   w.total = pos;
   return w;
 }
@@ -831,6 +848,7 @@ am_status blstm_teacher_forward(const am_model* m, const void* params, const voi
       f.G = at<void>(ws, w.g);
       f.sync = sync_slot(at<void>(ws, w.sync), k);
       f.err = sync_err(at<void>(ws, w.sync));
+      f.pre = at<float>(ws, w.pre);
       AM_TRY(forward_recurrence(f, sc, bf, H, s));
       AM_TRY(gather(at<void>(ws, w.hdir), H, out, 2 * H, d * H, (int)H, d == 1));
     }
@@ -952,6 +970,7 @@ am_status lstm_am_forward(const am_model* m, const void* params, const void* x,
     f.G = at<void>(ws, w.g[l]);
     f.sync = sync_slot(at<void>(ws, w.sync), l);
     f.err = sync_err(at<void>(ws, w.sync));
+    f.pre = at<float>(ws, w.pre);
     AM_TRY(forward_recurrence(f, sc, bf, H, s));
   }
   AM_TRY(run_gemm(AM_K_GEMM_FWD,
@@ -1081,7 +1100,7 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
         if (!used) tm.cancel();
       }
     }
-    if (!used) {
+    if (!used && !bf) {  // (the bf16 per-step path multiplies by Wh itself)
       Timed tm(AM_K_MISC, s, 0.0, 2.0 * G * H * e);
       AM_TRY(hip_check(am::transpose(P8 + po.wh[l] * e, WhT, (int)G, (int)H, bf, s), "Wh transpose"));
     }
@@ -1103,6 +1122,22 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
       a.nb = (int)nb;
       a.hidden = (int)H;
       a.bf16 = bf;
+      if (bf) {
+        // dA_{t+1} Wh as a batched product (few rows: square tiles), then
+        // the cell backward
+        // (k split up to four ways: the partials fill the [B][4H] fp32 scratch)
+        float* dhrec = at<float>(ws, w.pre);
+        int splits = 0;
+        if (nbn > 0) {
+          const am::GemmArgs g = mk_gemm(a.dAnext, G, true, P8 + po.wh[l] * e, H, false, dhrec, H,
+                                         true, nullptr, (int)nbn, (int)H, (int)G, true);
+          Timed tm(AM_K_LSTM_BWD, s, 2.0 * nbn * H * G, gemm_bytes(nbn, H, G, e, 4));
+          AM_TRY(hip_check(am::gemm_bf16_splitk_rows(g, 4, dhrec, &splits, s), "recurrent product"));
+        }
+        Timed tm(AM_K_LSTM_BWD, s, 0.0, (double)nb * (H * (4.0 * (splits > 0 ? splits : 1) + e + 16) + G * 2 * e));
+        AM_TRY(hip_check(am::lstm_cell_bwd(nbn > 0 ? dhrec : nullptr, splits, a, s), "lstm backward cell"));
+        continue;
+      }
       const double bytes = (double)(nbn * G + G * H + nb * H + nb * G) * e +
                            nb * H * 12.0 + (double)nb * G * e;
       Timed tm(AM_K_LSTM_BWD, s, 2.0 * nbn * G * H, bytes);

@@ -36,6 +36,8 @@
 // partial tiles, summed in split order by splitk_reduce in gemm.hip); for an
 // m-major A the first column of tiles also forms the row sums of A (the bias
 // gradient) with one more MFMA per row tile against a fragment of ones.
+#include <cstdlib>
+
 #include "am_device.h"
 #include "am_internal.h"
 
@@ -58,7 +60,10 @@ template <int BN, int BM> struct Cfg {
   static constexpr int A_BYTES = BM * BK * 2;
   static constexpr int B_BYTES = BN * BK * 2;
   static constexpr int STAGE = A_BYTES + B_BYTES;
-  static constexpr int NS = 3 * STAGE <= 150 * 1024 ? 3 : 2;  // LDS stages
+  // LDS stages: 3 (2 for the largest tiles); small tiles, whose k-tiles
+  // are short next to a memory round trip, keep up to 8 in flight
+  static constexpr int NS = STAGE <= 32 * 1024 ? (8 * STAGE <= 150 * 1024 ? 8 : 150 * 1024 / STAGE)
+                                               : (3 * STAGE <= 150 * 1024 ? 3 : 2);
   static constexpr int LDS = NS * STAGE;
   static constexpr int A_IPW = A_BYTES / 1024 / NW;  // direct loads per wave per tile
   static constexpr int B_IPW = B_BYTES / 1024 / NW;
@@ -263,7 +268,7 @@ __device__ __forceinline__ void store_tile_staged(const f32x4_t (&acc)[BM / 2 / 
 template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN, int BM>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
     Op A, Op B, Out<OutT> C, const bf16_t* __restrict__ bias, float* __restrict__ rowsum,
-    int M, int N, int K, int kps, int tm, int tn, int S, int staged) {
+    int M, int N, int K, int kps, int tm, int tn, int S, int flags) {
   using CF = Cfg<BN, BM>;
   extern __shared__ __align__(16) bf16_t smem[];
 
@@ -272,7 +277,11 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
   const int b = blockIdx.x, x = b % NX, q = G / NX, rem = G % NX;
   const int T = x * q + min(x, rem) + b / NX;
   const int z = T / (tm * tn), t2 = T % (tm * tn);
-  const int m0 = (t2 / tn) * BM, n0 = (t2 % tn) * BN;
+  // tile order: n fastest (consecutive tiles share rows of A), or, with
+  // few row tiles (flags & 2), m fastest (consecutive tiles share B)
+  const bool mfast = (flags & 2) != 0;
+  const int m0 = (mfast ? t2 % tm : t2 / tn) * BM, n0 = (mfast ? t2 / tm : t2 % tn) * BN;
+  const bool staged = (flags & 1) != 0;
   const int kbeg = z * kps, kend = min(K, kbeg + kps);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -399,7 +408,7 @@ hipError_t launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kp
   constexpr int lds = Cfg<BN, BM>::LDS;
   hipLaunchKernelGGL(kern, dim3(tm * tn * S), dim3(NT), lds, s, A, B, dst,
                      static_cast<const bf16_t*>(g.bias), rowsum, g.M, g.N, g.K, kps, tm, tn, S,
-                     staged ? 1 : 0);
+                     (staged ? 1 : 0) | (tm <= 8 && tn >= 2 * tm ? 2 : 0));
   return hipGetLastError();
 }
 
@@ -441,9 +450,29 @@ int pick_bn(int M, int N) {
   return t192 < t256 ? 192 : 256;
 }
 
+// Products with few rows (M <= 2048, e.g. one time step of the recurrence
+// run as a product): square tiles of 128 or 64 where 256-row tiles would
+// leave most CUs idle.  Relative time = rounds of one workgroup per CU x
+// tile area / efficiency (smaller tiles read more LDS bytes per flop).
+int pick_small(int M, int N) {
+  if (M > 2048) return 0;
+  int best = 0;
+  double tbest = 0.0;
+  const struct { int t; double eff; } cand[] = {{256, 1.0}, {128, 0.8}, {64, 0.55}};
+  for (const auto& c : cand) {
+    const int64_t tiles = (int64_t)((M + c.t - 1) / c.t) * ((N + c.t - 1) / c.t);
+    const double t = grid_time(tiles, (double)c.t * c.t / c.eff);
+    if (best == 0 || t < tbest) { best = c.t; tbest = t; }
+  }
+  return best == 256 ? 0 : best;
+}
+
 template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM>
 hipError_t launch_bn(int bn, const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kps,
                      hipStream_t s) {
+  const int sm = pick_small(g.M, g.N);
+  if (sm == 128) return launch<AK, BKM, OutT, BIAS, ROWSUM, 128, 128>(g, dst, rowsum, S, kps, s);
+  if (sm == 64) return launch<AK, BKM, OutT, BIAS, ROWSUM, 64, 64>(g, dst, rowsum, S, kps, s);
   return bn == 192 ? launch<AK, BKM, OutT, BIAS, ROWSUM, 192>(g, dst, rowsum, S, kps, s)
                    : launch<AK, BKM, OutT, BIAS, ROWSUM, 256>(g, dst, rowsum, S, kps, s);
 }
@@ -466,6 +495,22 @@ hipError_t weight_grads(const GemmArgs& g, int S, int ktiles, hipStream_t s) {
 }
 
 }  // namespace
+
+// C-partials [S][M][N] fp32 of a product with few rows and a long k-range
+// (A k-major, B n-major), K split S ways over 128 x 128 tiles: S = the most
+// splits (up to max_splits, at least 8 k-tiles each) that keep the grid
+// within one workgroup per CU.  Returns S through *splits.
+hipError_t gemm_bf16_splitk_rows(const GemmArgs& g, int max_splits, float* part, int* splits,
+                                 hipStream_t s) {
+  const int64_t tiles = (int64_t)((g.M + 127) / 128) * ((g.N + 127) / 128);
+  const int ktiles = (g.K + BK - 1) / BK;
+  int S = 1;
+  while (S < max_splits && tiles * (S + 1) <= device_cus() && ktiles / (S + 1) >= 8) ++S;
+  const int kps = ((ktiles + S - 1) / S) * BK;
+  Out<float> d{part, g.N, part, g.N, 1 << 30, (int64_t)g.M * g.N};
+  *splits = S;
+  return launch<true, false, float, false, false, 128, 128>(g, d, nullptr, S, kps, s);
+}
 
 hipError_t gemm_bf16(const GemmArgs& g, hipStream_t s) {
   if (g.a_kmajor && g.b_kmajor) {  // forward projections

@@ -211,7 +211,83 @@ __global__ __launch_bounds__(256) void lstm_bwd_step_kernel(
   }
 }
 
+// The cell of one step on its own (bf16 activations), after the recurrent
+// product of the step ran as a batched product into pre [nb][4H] fp32 (or
+// pre == null: a zero h_{t-1}).  One thread per (row, unit), consecutive
+// threads consecutive units.
+__global__ __launch_bounds__(256) void lstm_cell_fwd_kernel(
+    const float* __restrict__ pre, const bf16_t* __restrict__ P, const bf16_t* __restrict__ hprev,
+    const float* __restrict__ cprev, bf16_t* __restrict__ Hout, bf16_t* __restrict__ Hs,
+    float* __restrict__ Cout, bf16_t* __restrict__ G, int nb, int H) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (int64_t)nb * H) return;
+  const int64_t row = e / H;
+  const int j = (int)(e - row * H);
+  const int64_t G4 = 4 * (int64_t)H, pr = row * G4;
+  float a[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+    a[g] = (pre ? pre[pr + g * H + j] : 0.f) + bf16_to_f32(P[pr + g * H + j]);
+  const float gi = sigm(a[0]), gf = sigm(a[1]), gg = tanh_f(a[2]), go = sigm(a[3]);
+  const float c = gf * (cprev ? cprev[e] : 0.f) + gi * gg;
+  Cout[e] = c;
+  Hout[e] = f32_to_bf16(go * tanh_f(c));
+  Hs[e] = hprev ? hprev[e] : (bf16_t)0;
+  store_gates(G + pr, j, gi, gf, gg, go);
+}
+
+// The cell backward of one step: dh = dHa + dhrec (rows < nbn; dhrec holds
+// the `splits` k-split partials [splits][nbn][H] fp32 of the batched product
+// dA_{t+1} Wh, summed in split order), dc carried in dc.
+__global__ __launch_bounds__(256) void lstm_cell_bwd_kernel(
+    const float* __restrict__ dhrec, int splits, int nbn, const bf16_t* __restrict__ dHa,
+    const bf16_t* __restrict__ G, const float* __restrict__ C, const float* __restrict__ Cprev,
+    float* __restrict__ dc, bf16_t* __restrict__ dA, int nb, int H) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (int64_t)nb * H) return;
+  const int64_t row = e / H;
+  const int j = (int)(e - row * H);
+  const int64_t G4 = 4 * (int64_t)H;
+  bf16_t gv[4];
+  load_gates(G + row * G4, j, gv);
+  const float gi = bf16_to_f32(gv[0]), gf = bf16_to_f32(gv[1]);
+  const float gg = bf16_to_f32(gv[2]), go = bf16_to_f32(gv[3]);
+  const bool cont = row < nbn;  // the sequence continues to step t+1
+  float rec = 0.f;
+  if (cont)
+    for (int z = 0; z < splits; ++z) rec += dhrec[(int64_t)z * nbn * H + e];
+  const float dh = bf16_to_f32(dHa[e]) + rec;
+  const float tc = tanh_f(C[e]);
+  const float d_o = dh * tc;
+  const float dcell = dh * go * (1.f - tc * tc) + (cont ? dc[e] : 0.f);
+  const float d_i = dcell * gg, d_g = dcell * gi, d_f = dcell * (Cprev ? Cprev[e] : 0.f);
+  dc[e] = dcell * gf;
+  bf16_t* arow = dA + row * G4;
+  arow[j] = f32_to_bf16(d_i * gi * (1.f - gi));
+  arow[H + j] = f32_to_bf16(d_f * gf * (1.f - gf));
+  arow[2 * H + j] = f32_to_bf16(d_g * (1.f - gg * gg));
+  arow[3 * H + j] = f32_to_bf16(d_o * go * (1.f - go));
+}
+
 }  // namespace
+
+hipError_t lstm_cell_fwd(const float* pre, const LstmFwdStep& a, hipStream_t s) {
+  if (a.nb <= 0) return hipSuccess;
+  const int64_t cells = (int64_t)a.nb * a.hidden;
+  hipLaunchKernelGGL(lstm_cell_fwd_kernel, dim3((unsigned)((cells + 255) / 256)), dim3(256), 0, s,
+                     pre, (const bf16_t*)a.P, (const bf16_t*)a.hprev, a.cprev, (bf16_t*)a.H,
+                     (bf16_t*)a.Hs, a.C, (bf16_t*)a.G, a.nb, a.hidden);
+  return hipGetLastError();
+}
+
+hipError_t lstm_cell_bwd(const float* dhrec, int splits, const LstmBwdStep& a, hipStream_t s) {
+  if (a.nb <= 0) return hipSuccess;
+  const int64_t cells = (int64_t)a.nb * a.hidden;
+  hipLaunchKernelGGL(lstm_cell_bwd_kernel, dim3((unsigned)((cells + 255) / 256)), dim3(256), 0, s,
+                     dhrec, dhrec ? splits : 0, a.nbn, (const bf16_t*)a.dHa, (const bf16_t*)a.G, a.C, a.Cprev, a.dc,
+                     (bf16_t*)a.dA, a.nb, a.hidden);
+  return hipGetLastError();
+}
 
 hipError_t lstm_fwd_step(const LstmFwdStep& a, hipStream_t s) {
   if (a.nb <= 0) return hipSuccess;
