@@ -29,6 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+SAMPLE_EVERY = 7            # bracket one launch in 7 of the timed class (coprime to 5, 6, 635)
 PEAK_FP32_TFLOPS = 157.3    # MI355X dense fp32 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 METRIC = "training frames/sec on 1 MI355X (5x768 LSTM, 3000 senones); MFMA util %"
@@ -485,7 +486,10 @@ def measure(wl, steps, warmup, am, synth, trainer):
     dom = max(classes, key=lambda k: totals[k]["ms"])
     torch.cuda.synchronize()
 
-    am.profile_begin([dom])
+    # one bracketed launch in SAMPLE_EVERY: each bracket costs a few µs of
+    # queue time, and an interval coprime to the class's launches per step
+    # visits each of its launch positions in turn
+    am.profile_begin([dom], every=SAMPLE_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
@@ -515,7 +519,8 @@ def measure(wl, steps, warmup, am, synth, trainer):
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     roof["traffic"] = traffic_for(name, per_launch, wl)
     roof["kernel"] = name
-    roof["launches_per_step"] = kt["launches"] // steps
+    roof["launches_per_step"] = totals[dom]["launches"]
+    roof["sampled_launches"] = kt["launches"]
     roof["avg_launch_us"] = round(avg_ms * 1e3, 2)
     roof["algorithmic_per_launch"] = per_launch
     # the quantiser at the step's own send rate (the recorded step's encode:

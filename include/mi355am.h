@@ -354,6 +354,12 @@ typedef enum {
  * `class_mask` is bracketed by HIP events on its stream.  Clears earlier
  * records.  Not thread-safe; one recording at a time per process. */
 am_status am_profile_begin(uint32_t class_mask);
+/* Records only every n-th launch of each recorded class (n >= 1; 1, the
+ * default, records every launch), counted from am_profile_begin.  Each
+ * bracket adds a few microseconds of queue time between kernels; sampling
+ * with an n coprime to a class's launches per step still visits every
+ * launch position of the step.  Returns AM_EINVAL for n < 1. */
+am_status am_profile_sample_every(int32_t n);
 /* Stops recording and synchronises on the recorded events. */
 am_status am_profile_end(void);
 /* Totals for one class since am_profile_begin: launches, summed kernel

@@ -92,6 +92,7 @@ _PROTOS = {
     "am_workspace_check": (_I32, [_P, _I64, _P]),
     "am_profile_begin": (_I32, [ctypes.c_uint32]),
     "am_profile_end": (_I32, []),
+    "am_profile_sample_every": (_I32, [_I32]),
     "am_profile_get": (_I32, [_I32, _P, _P, _P, _P]),
 }
 
@@ -367,10 +368,13 @@ def cast_f32_to_bf16(src, dst, stream=None):
 
 # ------------------------------------------------------------------ timing --
 
-def profile_begin(classes):
+def profile_begin(classes, every=1):
+    """Brackets the launches of `classes` with HIP events; with every > 1
+    only every n-th launch of each class is bracketed."""
     mask = 0
     for k in classes:
         mask |= 1 << k
+    _check(lib().am_profile_sample_every(int(every)))
     _check(lib().am_profile_begin(mask))
 
 

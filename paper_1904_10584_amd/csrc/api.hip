@@ -51,6 +51,8 @@ struct ProfRec {
 struct Prof {
   bool on = false;
   uint32_t mask = 0;
+  int32_t every = 1;                    // record every n-th launch of a class
+  int64_t seen[AM_K_NCLASSES] = {};     // launches of the class since begin
   std::vector<hipEvent_t> pool;
   size_t next = 0;
   std::vector<ProfRec> recs;
@@ -60,20 +62,24 @@ struct Prof {
 
 hipEvent_t prof_event() {
   if (g_prof.next == g_prof.pool.size()) {
+    // timing only: no system-scope fence (cache write-back) at each record,
+    // which would otherwise add a gap of several microseconds per bracket
     hipEvent_t e;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     g_prof.pool.push_back(e);
   }
   return g_prof.pool[g_prof.next++];
 }
 
 // Brackets the kernels launched during its lifetime with events when the
-// class is being recorded.
+// class is being recorded (every n-th launch of the class when sampling).
 class Timed {
  public:
   Timed(int cls, hipStream_t s, double flops, double bytes) : s_(s) {
     if (!g_prof.on || !(g_prof.mask & (1u << cls))) return;
     rec_.cls = cls;
+    counted_ = true;
+    if (g_prof.seen[cls]++ % g_prof.every != 0) return;
     rec_.flops = flops;
     rec_.bytes = bytes;
     rec_.a = prof_event();
@@ -83,11 +89,15 @@ class Timed {
   ~Timed() {
     if (active_ && hipEventRecord(rec_.b, s_) == hipSuccess) g_prof.recs.push_back(rec_);
   }
-  void cancel() { active_ = false; }  // nothing was launched
+  void cancel() {  // nothing was launched
+    if (counted_) --g_prof.seen[rec_.cls];
+    counted_ = active_ = false;
+  }
 
  private:
   hipStream_t s_;
   ProfRec rec_{};
+  bool counted_ = false;
   bool active_ = false;
 };
 
@@ -1182,9 +1192,16 @@ am_status am_profile_begin(uint32_t class_mask) {
   g_prof.next = 0;
   g_prof.recs.clear();
   for (int k = 0; k < AM_K_NCLASSES; ++k) {
+    g_prof.seen[k] = 0;
     g_prof.launches[k] = 0;
     g_prof.ms[k] = g_prof.flops[k] = g_prof.bytes[k] = 0.0;
   }
+  return AM_OK;
+}
+
+am_status am_profile_sample_every(int32_t n) {
+  if (n < 1) return fail(AM_EINVAL, "sampling interval must be at least 1");
+  g_prof.every = n;
   return AM_OK;
 }
 

@@ -216,3 +216,11 @@ def test_recurrence_path_query(monkeypatch):
     assert am.recurrence_path(paper, 64, 256) == am.PATH_STEP
     with pytest.raises(am.AmError):
         am.recurrence_path(am.Model(5, 192, 770, 3000, am.BF16), 64, 256)
+
+
+def test_profile_sampling_interval(L):
+    # host logic only (no launch is recorded): the interval must be >= 1
+    assert L.am_profile_sample_every(0) == am.EINVAL
+    assert L.am_profile_sample_every(-3) == am.EINVAL
+    assert L.am_profile_sample_every(7) == am.OK
+    assert L.am_profile_sample_every(1) == am.OK
