@@ -37,6 +37,7 @@
 // m-major A the first column of tiles also forms the row sums of A (the bias
 // gradient) with one more MFMA per row tile against a fragment of ones.
 #include <cstdlib>
+#include <type_traits>
 
 #include "am_device.h"
 #include "am_internal.h"
@@ -114,19 +115,37 @@ __device__ __forceinline__ const bf16_t* op_ptr(const Op& o, int row, int k, boo
   return kmajor ? p + (int64_t)r * ld + k : p + (int64_t)k * ld + r;
 }
 
-// Issue direct load j of this wave for one R-row operand tile (R * BK * 2
-// bytes in R / 8 loads of 1 KiB, R / 8 / NW per wave).
-template <bool KMAJOR, int R>
-__device__ __forceinline__ void dma_one(const Op& o, int row0, int nrows, int k0, int kend,
-                                        const bf16_t* lds, int wave, int lane, int j) {
-  {
+// Direct loads of one R-row operand tile: R * BK * 2 bytes in R / 8 loads of
+// 1 KiB, R / 8 / NW per wave.  A k-major load fetches 8 rows x 8 chunks; an
+// m/n-major load k-rows of R / 8 chunks laid end to end.  A load whose row
+// is outside the operand, or whose k index has passed kend, reads the zero
+// vector.  Two ways to address them:
+//   * DirectLoader works out each address at the issue;
+//   * TileLoader works them out once per workgroup: load j of this wave
+//     keeps its source pointer and k index, and each issue advances both by
+//     one k-tile (a load is issued once per k-tile, in k-tile order).  Used
+//     where both operands are m/n-major (the weight gradients: 7 % faster);
+//     on the other products the extra live registers cost more than the
+//     address arithmetic they save.
+template <bool KMAJOR, int R, int NL>
+struct DirectLoader {
+  Op o;
+  int row0, nrows;
+
+  __device__ __forceinline__ void init(const Op& o_, int row0_, int nrows_, int, int, int) {
+    o = o_;
+    row0 = row0_;
+    nrows = nrows_;
+  }
+  __device__ __forceinline__ void issue(int j, int k0, int kend, const bf16_t* lds, int wave,
+                                        int lane) {
     const int q = wave + NW * j;
     int row, k;
-    if (KMAJOR) {  // 8 rows x 8 chunks per load
+    if (KMAJOR) {
       const int r = 8 * q + (lane >> 3);
       row = row0 + r;
       k = k0 + (((lane & 7) ^ (r & 7)) << 3);
-    } else {       // k-rows of R / 8 chunks, laid end to end
+    } else {
       constexpr int CPR = R / 8;
       const int e = q * 64 + lane;  // chunk index in the tile
       const int kr = e / CPR;
@@ -137,7 +156,50 @@ __device__ __forceinline__ void dma_one(const Op& o, int row0, int nrows, int k0
     const void* src = ok ? (const void*)op_ptr(o, row, k, KMAJOR) : (const void*)g_zero;
     dma16(src, __builtin_amdgcn_readfirstlane(lds_address(lds + q * 512)));
   }
-}
+};
+
+template <bool KMAJOR, int R, int NL>
+struct TileLoader {
+  static constexpr int L = NL > 0 ? NL : 1;
+  const bf16_t* p[L];
+  int kk[L];
+  int inc[L];  // elements per k-tile (m-major: BK rows of the lane's source)
+
+  __device__ __forceinline__ void init(const Op& o, int row0, int nrows, int k0, int wave,
+                                       int lane) {
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+      const int q = wave + NW * j;
+      int row, k;
+      if (KMAJOR) {
+        const int r = 8 * q + (lane >> 3);
+        row = row0 + r;
+        k = k0 + (((lane & 7) ^ (r & 7)) << 3);
+      } else {
+        constexpr int CPR = R / 8;
+        const int e = q * 64 + lane;
+        const int kr = e / CPR;
+        k = k0 + kr;
+        row = row0 + (((e % CPR) ^ ((kr & 3) << 1)) << 3);
+      }
+      const bool sec = row >= o.split;
+      const bf16_t* base = sec ? o.p1 : o.p0;
+      const int64_t ld = sec ? o.ld1 : o.ld0;
+      const int r = sec ? row - o.split : row;
+      const bool in = row < nrows;
+      p[j] = in ? (KMAJOR ? base + (int64_t)r * ld + k : base + (int64_t)k * ld + r) : base;
+      kk[j] = in ? k : (1 << 30);
+      inc[j] = KMAJOR ? BK : (int)(BK * ld);
+    }
+  }
+  __device__ __forceinline__ void issue(int j, int, int kend, const bf16_t* lds, int wave, int) {
+    const int q = wave + NW * j;
+    const void* src = kk[j] < kend ? (const void*)p[j] : (const void*)g_zero;
+    dma16(src, __builtin_amdgcn_readfirstlane(lds_address(lds + q * 512)));
+    p[j] += KMAJOR ? BK : inc[j];
+    kk[j] += BK;
+  }
+};
 
 // Fragment of rows/columns r0 .. r0+15, k-step ks of an R-row tile.
 template <bool KMAJOR, int R>
@@ -300,12 +362,22 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
   ones.v = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
 
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
-  // direct load `idx` (< IPW) of this wave for k-tile t
+  constexpr bool PRE = !AK && !BKM;
+  using LA = typename std::conditional<PRE, TileLoader<AK, BM, CF::A_IPW>,
+                                       DirectLoader<AK, BM, CF::A_IPW>>::type;
+  using LB = typename std::conditional<PRE, TileLoader<BKM, BN, CF::B_IPW>,
+                                       DirectLoader<BKM, BN, CF::B_IPW>>::type;
+  LA lda;
+  LB ldb;
+  lda.init(A, m0, M, kbeg, wave, lane);
+  ldb.init(B, n0, N, kbeg, wave, lane);
+  // direct load `idx` (< IPW) of this wave for k-tile t (each idx is issued
+  // once per k-tile, in k-tile order)
   auto dma = [&](int t, int idx) {
     const bf16_t* st = smem + (t % CF::NS) * (CF::STAGE / 2);
-    if (idx < CF::A_IPW) dma_one<AK, BM>(A, m0, M, kbeg + t * BK, kend, st, wave, lane, idx);
-    else dma_one<BKM, BN>(B, n0, N, kbeg + t * BK, kend, st + CF::A_BYTES / 2, wave, lane,
-                          idx - CF::A_IPW);
+    const int k0 = kbeg + t * BK;
+    if (idx < CF::A_IPW) lda.issue(idx, k0, kend, st, wave, lane);
+    else ldb.issue(idx - CF::A_IPW, k0, kend, st + CF::A_BYTES / 2, wave, lane);
   };
 #pragma unroll
   for (int p = 0; p < CF::NS - 1; ++p)
@@ -382,11 +454,11 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
 template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN, int BM = BM0>
 hipError_t launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kps, hipStream_t s) {
   auto kern = gemm_bf16_kernel<AK, BKM, OutT, BIAS, ROWSUM, BN, BM>;
+  constexpr int lds = Cfg<BN, BM>::LDS;
   static bool attr = false;  // per instantiation
   if (!attr) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             Cfg<BN, BM>::LDS);
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     attr = true;
   }
@@ -405,7 +477,6 @@ hipError_t launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kp
   const bool staged = (al & 15) == 0 && g.N % EPC == 0 && dst.ld0 % EPC == 0 &&
                       dst.ld1 % EPC == 0 && (dst.split >= g.N || dst.split % EPC == 0) &&
                       dst.zstride % EPC == 0 && (sizeof(OutT) == 2 || S == 1);
-  constexpr int lds = Cfg<BN, BM>::LDS;
   hipLaunchKernelGGL(kern, dim3(tm * tn * S), dim3(NT), lds, s, A, B, dst,
                      static_cast<const bf16_t*>(g.bias), rowsum, g.M, g.N, g.K, kps, tm, tn, S,
                      (staged ? 1 : 0) | (tm <= 8 && tn >= 2 * tm ? 2 : 0));
