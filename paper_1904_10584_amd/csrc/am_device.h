@@ -118,6 +118,28 @@ __device__ __forceinline__ float sigm(float x) {
 }
 __device__ __forceinline__ float tanh_f(float x) { return 2.0f * sigm(2.0f * x) - 1.0f; }
 
+// One LSTM cell step of one unit (bf16 per-step paths) from its gate
+// pre-activations (i, f, g, o) and c_{t-1}: the gates, c_t and h_t.  The
+// products are rounded separately (no multiply-add contraction), so every
+// kernel that calls this gets the same bits from the same inputs.
+struct CellStep {
+  float gi, gf, gg, go, c, h;
+};
+__device__ __forceinline__ CellStep lstm_cell_step(float a0, float a1, float a2, float a3,
+                                                   float cprev) {
+#pragma clang fp contract(off)
+  CellStep r;
+  r.gi = sigm(a0);
+  r.gf = sigm(a1);
+  r.gg = tanh_f(a2);
+  r.go = sigm(a3);
+  const float keep = r.gf * cprev;
+  const float add = r.gi * r.gg;
+  r.c = keep + add;
+  r.h = r.go * tanh_f(r.c);
+  return r;
+}
+
 // Byte address of an LDS object (for instructions that take it in M0).
 __device__ __forceinline__ uint32_t lds_address(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;

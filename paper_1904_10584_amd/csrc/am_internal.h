@@ -30,6 +30,14 @@ struct GemmArgs {
   float* ws = nullptr; int64_t ws_floats = 0;
 };
 hipError_t gemm(const GemmArgs& g, hipStream_t s);
+// One forward LSTM step as one launch: the recurrent product h_{t-1} Wh^T
+// with the cell in its epilogue (bf16, products of at most 2048 rows; W_h's
+// gate rows are read interleaved, so each output tile holds all four gates
+// of its units).  Same results, bit for bit, as the product into fp32
+// scratch followed by lstm_cell_fwd.  *done = false: not covered (nothing
+// launched; the caller runs the two-launch form).
+struct LstmFwdStep;
+hipError_t gemm_bf16_lstm_fwd_step(const LstmFwdStep& a, hipStream_t s, bool* done);
 // The bf16 products (gemm routes bf16 arguments here).
 hipError_t gemm_bf16(const GemmArgs& g, hipStream_t s);
 // A k-major, B n-major, K split up to max_splits ways: fp32 partials

@@ -185,6 +185,14 @@ bool persistent_enabled() {
   return !(r && strcmp(r, "step") == 0);
 }
 
+// The bf16 per-step forward runs each step as one launch with the cell in
+// the product's epilogue; AM_STEP_FUSION=0 in the environment keeps the
+// product and the cell as two launches (tests compare the two bit for bit).
+bool step_cell_fusion() {
+  const char* v = getenv("AM_STEP_FUSION");
+  return !(v && v[0] == '0' && v[1] == 0);
+}
+
 // AM_RECURRENCE=xcd|device|step picks one recurrence path (for tests);
 // unset, the XCD-local kernels are tried first, then the device-scope ones.
 bool xcd_enabled() {
@@ -205,6 +213,9 @@ bool device_persistent_enabled() {
 // so a time-out anywhere in a forward + backward pair stays visible to
 // am_workspace_check.
 constexpr int64_t SYNC_BYTES = 8192;
+// k-splits of the per-step backward product dA_{t+1} W_h (five fill 240 of
+// the 256 CUs with the 48 tiles of B = 512, H = 1536)
+constexpr int STEP_SPLITS = 5;
 constexpr int64_t SYNC_STICKY_WORD = SYNC_BYTES / 4 - 1;
 void* sync_slot(void* area, int k) { return static_cast<char*>(area) + (int64_t)k * SYNC_BYTES; }
 int* sync_err(void* area) { return static_cast<int*>(area) + SYNC_STICKY_WORD; }
@@ -283,7 +294,9 @@ WsLayout ws_layout(const am_model* m, int64_t B, int64_t N) {
   w.dc = take(B * H * 4);
   w.c0 = take(L * B * H * 4);
   w.h0 = take(L * B * H * e);
-  w.pre = take(B * G * 4);  // one step's recurrent product (per-step path)
+  // one step's recurrent product (per-step path): [B][4H] fp32 forward, up to
+  // STEP_SPLITS k-split partials [B][H] fp32 backward
+  w.pre = take(B * H * 4 * (STEP_SPLITS > 4 ? STEP_SPLITS : 4));
   // split-K partials of the weight-gradient products (plus partial row sums)
   const int64_t D0 = m->input_dim;
   const int64_t wide = (D0 > H ? D0 : H) + H;
@@ -370,6 +383,7 @@ am_status forward_recurrence(const FwdLayer& f, const Schedule& sc, bool bf, int
   }
   const char* Hl = static_cast<const char*>(f.H);
   const float* Cl = f.C;
+  const bool fuse_cell = step_cell_fusion();
   for (int t = 0; t < T; ++t) {
     const int64_t nb = sc.counts[t];
     if (nb == 0) break;
@@ -393,8 +407,17 @@ am_status forward_recurrence(const FwdLayer& f, const Schedule& sc, bool bf, int
     a.bf16 = bf;
     if (bf) {
       // the step's recurrent product as a batched product (few rows: square
-      // tiles that fill the CUs), then the cell
+      // tiles that fill the CUs) with the cell in its epilogue; else the
+      // product into fp32 scratch, then the cell
       float* pre = nullptr;
+      if (a.hprev && fuse_cell) {
+        bool done = false;
+        Timed tm(AM_K_LSTM_FWD, s, 2.0 * nb * G * H,
+                 gemm_bytes(nb, G, H, e, 0) + (double)nb * (G * e + H * (2 * e + 8) + G * e));
+        AM_TRY(hip_check(am::gemm_bf16_lstm_fwd_step(a, s, &done), "lstm forward step (fused)"));
+        if (done) continue;
+        tm.cancel();
+      }
       if (a.hprev) {
         AM_TRY(run_gemm(AM_K_LSTM_FWD,
                         mk_gemm(a.hprev, H, true, f.Wh, H, true, f.pre, G, true, nullptr, (int)nb,
@@ -1135,14 +1158,14 @@ am_status lstm_am_backward(const am_model* m, const void* params, const void* x,
       if (bf) {
         // dA_{t+1} Wh as a batched product (few rows: square tiles), then
         // the cell backward
-        // (k split up to four ways: the partials fill the [B][4H] fp32 scratch)
+        // (k split up to STEP_SPLITS ways: the partials fill the fp32 scratch)
         float* dhrec = at<float>(ws, w.pre);
         int splits = 0;
         if (nbn > 0) {
           const am::GemmArgs g = mk_gemm(a.dAnext, G, true, P8 + po.wh[l] * e, H, false, dhrec, H,
                                          true, nullptr, (int)nbn, (int)H, (int)G, true);
           Timed tm(AM_K_LSTM_BWD, s, 2.0 * nbn * H * G, gemm_bytes(nbn, H, G, e, 4));
-          AM_TRY(hip_check(am::gemm_bf16_splitk_rows(g, 4, dhrec, &splits, s), "recurrent product"));
+          AM_TRY(hip_check(am::gemm_bf16_splitk_rows(g, STEP_SPLITS, dhrec, &splits, s), "recurrent product"));
         }
         Timed tm(AM_K_LSTM_BWD, s, 0.0, (double)nb * (H * (4.0 * (splits > 0 ? splits : 1) + e + 16) + G * 2 * e));
         AM_TRY(hip_check(am::lstm_cell_bwd(nbn > 0 ? dhrec : nullptr, splits, a, s), "lstm backward cell"));

@@ -107,6 +107,18 @@ struct Op {
   int split;
 };
 
+// Arguments of the LSTM cell epilogue (CELL kernels): the rows of step t.
+struct CellArgs {
+  const bf16_t* P;      // [nb][4H] input projection + bias
+  const bf16_t* hprev;  // [nb][H] h_{t-1}
+  const float* cprev;   // [nb][H] c_{t-1}, or null
+  bf16_t* H;            // [nb][H] h_t
+  bf16_t* Hs;           // [nb][H] copy of h_{t-1}
+  float* C;             // [nb][H] c_t
+  bf16_t* G;            // [nb][H][4] gates
+  int hidden;
+};
+
 __device__ __forceinline__ const bf16_t* op_ptr(const Op& o, int row, int k, bool kmajor) {
   const bool sec = row >= o.split;
   const bf16_t* p = sec ? o.p1 : o.p0;
@@ -127,15 +139,17 @@ __device__ __forceinline__ const bf16_t* op_ptr(const Op& o, int row, int k, boo
 //     where both operands are m/n-major (the weight gradients: 7 % faster);
 //     on the other products the extra live registers cost more than the
 //     address arithmetic they save.
-template <bool KMAJOR, int R, int NL>
+template <bool KMAJOR, int R, int NL, bool GI = false>
 struct DirectLoader {
   Op o;
-  int row0, nrows;
+  int row0, nrows, gh;
 
-  __device__ __forceinline__ void init(const Op& o_, int row0_, int nrows_, int, int, int) {
+  __device__ __forceinline__ void init(const Op& o_, int row0_, int nrows_, int, int, int,
+                                       int gh_ = 0) {
     o = o_;
     row0 = row0_;
     nrows = nrows_;
+    gh = gh_;
   }
   __device__ __forceinline__ void issue(int j, int k0, int kend, const bf16_t* lds, int wave,
                                         int lane) {
@@ -153,7 +167,9 @@ struct DirectLoader {
       row = row0 + (((e % CPR) ^ ((kr & 3) << 1)) << 3);
     }
     const bool ok = row < nrows && k < kend;
-    const void* src = ok ? (const void*)op_ptr(o, row, k, KMAJOR) : (const void*)g_zero;
+    // gate-interleaved: tile row 4u + g is operand row g * gh + u
+    const int mrow = GI ? (row & 3) * gh + (row >> 2) : row;
+    const void* src = ok ? (const void*)op_ptr(o, mrow, k, KMAJOR) : (const void*)g_zero;
     dma16(src, __builtin_amdgcn_readfirstlane(lds_address(lds + q * 512)));
   }
 };
@@ -325,12 +341,95 @@ __device__ __forceinline__ void store_tile_staged(const f32x4_t (&acc)[BM / 2 / 
   }
 }
 
+// LSTM cell epilogue of a gate-interleaved tile (column 4u + g is gate g of
+// unit n0 / 4 + u).  Each thread takes ITEMS (row, unit) items, consecutive
+// threads consecutive units of one row.  After the k-loop the items'
+// operands that do not depend on the product (the input projection's four
+// gates, c_{t-1}, h_{t-1}) are all loaded at once (cell_load), while the
+// fp32 accumulators (the recurrent part of the gate pre-activations) go to
+// LDS in row-major order; then each item runs the cell (cell_finish, with
+// lstm_cell_step as lstm_cell_fwd_kernel).  Needs BM x (BN +
+// 4) x 4 bytes of LDS.
+template <int BN, int BM> struct CellItems {
+  static constexpr int UPR = BN / 4;                 // units per tile row
+  static constexpr int ITEMS = BM * UPR / NT;
+  static_assert(BM * UPR % NT == 0, "items per thread");
+  uint32_t p01[ITEMS], p23[ITEMS];  // P's gates (i, f) and (g, o) as bf16 pairs
+  float cp[ITEMS];
+  bf16_t hp[ITEMS];
+};
+
+template <int BN, int BM>
+__device__ __forceinline__ void cell_load(CellItems<BN, BM>& it, const CellArgs& c, int M,
+                                          int m0, int n0) {
+  using CI = CellItems<BN, BM>;
+  const int H = c.hidden;
+#pragma unroll
+  for (int q = 0; q < CI::ITEMS; ++q) {
+    const int e = threadIdx.x + q * NT;
+    const int row = m0 + e / CI::UPR, j = n0 / 4 + e % CI::UPR;
+    it.p01[q] = it.p23[q] = 0u;
+    it.cp[q] = 0.f;
+    it.hp[q] = 0;
+    if (row < M && j < H) {
+      const bf16_t* pr = c.P + (int64_t)row * 4 * H + j;
+      it.p01[q] = (uint32_t)pr[0] | ((uint32_t)pr[H] << 16);
+      it.p23[q] = (uint32_t)pr[2 * H] | ((uint32_t)pr[3 * H] << 16);
+      const int64_t o = (int64_t)row * H + j;
+      if (c.cprev) it.cp[q] = c.cprev[o];
+      it.hp[q] = c.hprev[o];
+    }
+  }
+}
+
+template <int BN, int BM>
+__device__ __forceinline__ void cell_finish(const f32x4_t (&acc)[BM / 2 / 16][BN / 4 / 16],
+                                            const CellItems<BN, BM>& it, const CellArgs& c,
+                                            bf16_t* smem, int M, int m0, int n0, int wm, int wn,
+                                            int lane) {
+  using CI = CellItems<BN, BM>;
+  constexpr int MI = BM / 2 / 16, NJ = BN / 4 / 16;
+  constexpr int ROWF = BN + 4;  // floats per LDS row (padded against bank conflicts)
+  float* lds = reinterpret_cast<float*>(smem);
+  __syncthreads();  // every wave is done with the stage buffers
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int cl = wn + j * 16 + mfma_col(lane);
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) lds[(wm + i * 16 + mfma_row(lane, r)) * ROWF + cl] = acc[i][j][r];
+  }
+  __syncthreads();
+  const int H = c.hidden;
+#pragma unroll
+  for (int q = 0; q < CI::ITEMS; ++q) {
+    const int e = threadIdx.x + q * NT;
+    const int rl = e / CI::UPR, u = e % CI::UPR;
+    const int row = m0 + rl, j = n0 / 4 + u;
+    if (row >= M || j >= H) continue;
+    const float4 rec = *reinterpret_cast<const float4*>(lds + rl * ROWF + 4 * u);
+    const float a0 = rec.x + bf16_to_f32((bf16_t)(it.p01[q] & 0xFFFFu));
+    const float a1 = rec.y + bf16_to_f32((bf16_t)(it.p01[q] >> 16));
+    const float a2 = rec.z + bf16_to_f32((bf16_t)(it.p23[q] & 0xFFFFu));
+    const float a3 = rec.w + bf16_to_f32((bf16_t)(it.p23[q] >> 16));
+    const CellStep cs = lstm_cell_step(a0, a1, a2, a3, it.cp[q]);
+    const int64_t o = (int64_t)row * H + j;
+    c.C[o] = cs.c;
+    c.H[o] = f32_to_bf16(cs.h);
+    c.Hs[o] = it.hp[q];
+    store_gates(c.G + (int64_t)row * 4 * H, j, cs.gi, cs.gf, cs.gg, cs.go);
+  }
+}
+
 // ROWSUM: A is m-major; the workgroups of the first column of tiles write
 // the row sums of A over their split's k-range to rowsum[z * M + m].
-template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN, int BM>
+// CELL: the LSTM cell epilogue (B's rows gate-interleaved; C unused).
+template <bool AK, bool BKM, typename OutT, bool BIAS, bool ROWSUM, int BN, int BM,
+          bool CELL = false>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
     Op A, Op B, Out<OutT> C, const bf16_t* __restrict__ bias, float* __restrict__ rowsum,
-    int M, int N, int K, int kps, int tm, int tn, int S, int flags) {
+    int M, int N, int K, int kps, int tm, int tn, int S, int flags, CellArgs cell) {
   using CF = Cfg<BN, BM>;
   extern __shared__ __align__(16) bf16_t smem[];
 
@@ -366,11 +465,12 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
   using LA = typename std::conditional<PRE, TileLoader<AK, BM, CF::A_IPW>,
                                        DirectLoader<AK, BM, CF::A_IPW>>::type;
   using LB = typename std::conditional<PRE, TileLoader<BKM, BN, CF::B_IPW>,
-                                       DirectLoader<BKM, BN, CF::B_IPW>>::type;
+                                       DirectLoader<BKM, BN, CF::B_IPW, CELL>>::type;
   LA lda;
   LB ldb;
   lda.init(A, m0, M, kbeg, wave, lane);
-  ldb.init(B, n0, N, kbeg, wave, lane);
+  if constexpr (CELL) ldb.init(B, n0, N, kbeg, wave, lane, cell.hidden);
+  else ldb.init(B, n0, N, kbeg, wave, lane);
   // direct load `idx` (< IPW) of this wave for k-tile t (each idx is issued
   // once per k-tile, in k-tile order)
   auto dma = [&](int t, int idx) {
@@ -428,6 +528,14 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
       }
   }
 
+  if constexpr (CELL) {
+    // (loaded only now: ordinary loads in flight during the k-loop would
+    // share vmcnt with the direct loads its partial waits count)
+    CellItems<BN, BM> items;
+    cell_load<BN, BM>(items, cell, M, m0, n0);
+    cell_finish<BN, BM>(acc, items, cell, smem, M, m0, n0, wm, wn, lane);
+    return;
+  }
   if (staged) {
     store_tile_staged<OutT, BN, BM, BIAS>(acc, C, bias, smem, M, N, m0, n0, z, wm, wn, wave, lane);
     return;
@@ -479,7 +587,32 @@ hipError_t launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kp
                       dst.zstride % EPC == 0 && (sizeof(OutT) == 2 || S == 1);
   hipLaunchKernelGGL(kern, dim3(tm * tn * S), dim3(NT), lds, s, A, B, dst,
                      static_cast<const bf16_t*>(g.bias), rowsum, g.M, g.N, g.K, kps, tm, tn, S,
-                     (staged ? 1 : 0) | (tm <= 8 && tn >= 2 * tm ? 2 : 0));
+                     (staged ? 1 : 0) | (tm <= 8 && tn >= 2 * tm ? 2 : 0), CellArgs{});
+  return hipGetLastError();
+}
+
+// The forward step with the cell in the epilogue: A = h_{t-1} [nb][H], B =
+// W_h [4H][H] read gate-interleaved, square tiles of pick_small's size.
+template <int T>
+hipError_t launch_cell(const GemmArgs& g, const CellArgs& cell, hipStream_t s) {
+  auto kern = gemm_bf16_kernel<true, true, float, false, false, T, T, true>;
+  constexpr int lds = Cfg<T, T>::LDS;
+  static_assert(T * (T + 4) * 4 <= lds, "the cell epilogue stages the fp32 tile in LDS");
+  static bool attr = false;
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const bf16_t* a = static_cast<const bf16_t*>(g.A);
+  const bf16_t* b = static_cast<const bf16_t*>(g.B);
+  Op A{a, g.lda, a, g.lda, 1 << 30};
+  Op B{b, g.ldb, b, g.ldb, 1 << 30};
+  const int tm = (g.M + T - 1) / T, tn = (g.N + T - 1) / T;
+  Out<float> none{nullptr, 0, nullptr, 0, 1 << 30, 0};
+  hipLaunchKernelGGL(kern, dim3(tm * tn), dim3(NT), lds, s, A, B, none, nullptr, nullptr, g.M,
+                     g.N, g.K, g.K, tm, tn, 1, (tm <= 8 && tn >= 2 * tm ? 2 : 0), cell);
   return hipGetLastError();
 }
 
@@ -581,6 +714,23 @@ hipError_t gemm_bf16_splitk_rows(const GemmArgs& g, int max_splits, float* part,
   Out<float> d{part, g.N, part, g.N, 1 << 30, (int64_t)g.M * g.N};
   *splits = S;
   return launch<true, false, float, false, false, 128, 128>(g, d, nullptr, S, kps, s);
+}
+
+hipError_t gemm_bf16_lstm_fwd_step(const LstmFwdStep& a, hipStream_t s, bool* done) {
+  *done = false;
+  const int H = a.hidden;
+  if (!a.bf16 || !a.hprev || a.nb <= 0 || H % 8 != 0) return hipSuccess;
+  const int sm = pick_small(a.nb, 4 * H);
+  if (sm != 128 && sm != 64) return hipSuccess;
+  GemmArgs g;
+  g.A = a.hprev; g.lda = H;
+  g.B = a.Wh; g.ldb = H;
+  g.M = a.nb; g.N = 4 * H; g.K = H; g.bf16 = true;
+  const CellArgs cell{static_cast<const bf16_t*>(a.P), static_cast<const bf16_t*>(a.hprev), a.cprev,
+                      static_cast<bf16_t*>(a.H), static_cast<bf16_t*>(a.Hs), a.C,
+                      static_cast<bf16_t*>(a.G), H};
+  *done = true;
+  return sm == 128 ? launch_cell<128>(g, cell, s) : launch_cell<64>(g, cell, s);
 }
 
 hipError_t gemm_bf16(const GemmArgs& g, hipStream_t s) {

@@ -228,12 +228,11 @@ __global__ __launch_bounds__(256) void lstm_cell_fwd_kernel(
 #pragma unroll
   for (int g = 0; g < 4; ++g)
     a[g] = (pre ? pre[pr + g * H + j] : 0.f) + bf16_to_f32(P[pr + g * H + j]);
-  const float gi = sigm(a[0]), gf = sigm(a[1]), gg = tanh_f(a[2]), go = sigm(a[3]);
-  const float c = gf * (cprev ? cprev[e] : 0.f) + gi * gg;
-  Cout[e] = c;
-  Hout[e] = f32_to_bf16(go * tanh_f(c));
+  const CellStep cs = lstm_cell_step(a[0], a[1], a[2], a[3], cprev ? cprev[e] : 0.f);
+  Cout[e] = cs.c;
+  Hout[e] = f32_to_bf16(cs.h);
   Hs[e] = hprev ? hprev[e] : (bf16_t)0;
-  store_gates(G + pr, j, gi, gf, gg, go);
+  store_gates(G + pr, j, cs.gi, cs.gf, cs.gg, cs.go);
 }
 
 // The cell backward of one step: dh = dHa + dhrec (rows < nbn; dhrec holds
