@@ -529,8 +529,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
   }
 
   if constexpr (CELL) {
-    // (loaded only now: ordinary loads in flight during the k-loop would
-    // share vmcnt with the direct loads its partial waits count)
+    // (loaded only now: the k-loop's partial vmcnt waits count its direct
+    // loads alone; ordinary loads in flight there would have to be counted
+    // in, relying on their order of return relative to the direct loads)
     CellItems<BN, BM> items;
     cell_load<BN, BM>(items, cell, M, m0, n0);
     cell_finish<BN, BM>(acc, items, cell, smem, M, m0, n0, wm, wn, lane);
