@@ -348,7 +348,10 @@ __device__ __forceinline__ void store_tile_staged(const f32x4_t (&acc)[BM / 2 / 
 // gates, c_{t-1}, h_{t-1}) are all loaded at once (cell_load), while the
 // fp32 accumulators (the recurrent part of the gate pre-activations) go to
 // LDS in row-major order; then each item runs the cell (cell_finish, with
-// lstm_cell_step as lstm_cell_fwd_kernel).  Needs BM x (BN +
+// lstm_cell_step as lstm_cell_fwd_kernel).  The epilogue's one-time reads
+// and the outputs kept for the backward are non-temporal: each XCD's tiles
+// share a fixed slice of W_h's rows (2.4 MB at H = 1536, B = 512), which
+// then stays in that XCD's L2 from one step to the next.  Needs BM x (BN +
 // 4) x 4 bytes of LDS.
 template <int BN, int BM> struct CellItems {
   static constexpr int UPR = BN / 4;                 // units per tile row
@@ -372,11 +375,14 @@ __device__ __forceinline__ void cell_load(CellItems<BN, BM>& it, const CellArgs&
     it.cp[q] = 0.f;
     it.hp[q] = 0;
     if (row < M && j < H) {
+      // (read once: non-temporal, so that they do not evict W_h's rows)
       const bf16_t* pr = c.P + (int64_t)row * 4 * H + j;
-      it.p01[q] = (uint32_t)pr[0] | ((uint32_t)pr[H] << 16);
-      it.p23[q] = (uint32_t)pr[2 * H] | ((uint32_t)pr[3 * H] << 16);
+      it.p01[q] = (uint32_t)__builtin_nontemporal_load(pr) |
+                  ((uint32_t)__builtin_nontemporal_load(pr + H) << 16);
+      it.p23[q] = (uint32_t)__builtin_nontemporal_load(pr + 2 * H) |
+                  ((uint32_t)__builtin_nontemporal_load(pr + 3 * H) << 16);
       const int64_t o = (int64_t)row * H + j;
-      if (c.cprev) it.cp[q] = c.cprev[o];
+      if (c.cprev) it.cp[q] = __builtin_nontemporal_load(c.cprev + o);
       it.hp[q] = c.hprev[o];
     }
   }
@@ -415,10 +421,15 @@ __device__ __forceinline__ void cell_finish(const f32x4_t (&acc)[BM / 2 / 16][BN
     const float a3 = rec.w + bf16_to_f32((bf16_t)(it.p23[q] >> 16));
     const CellStep cs = lstm_cell_step(a0, a1, a2, a3, it.cp[q]);
     const int64_t o = (int64_t)row * H + j;
-    c.C[o] = cs.c;
+    // h_t is the next step's operand; c_t, the h_{t-1} copy and the gates
+    // wait for the backward: non-temporal
+    __builtin_nontemporal_store(cs.c, c.C + o);
     c.H[o] = f32_to_bf16(cs.h);
-    c.Hs[o] = it.hp[q];
-    store_gates(c.G + (int64_t)row * 4 * H, j, cs.gi, cs.gf, cs.gg, cs.go);
+    __builtin_nontemporal_store(it.hp[q], c.Hs + o);
+    const uint2 pk = pack_gates(cs.gi, cs.gf, cs.gg, cs.go);
+    uint32_t* gp = reinterpret_cast<uint32_t*>(c.G + (int64_t)row * 4 * H + 4 * j);
+    __builtin_nontemporal_store(pk.x, gp);
+    __builtin_nontemporal_store(pk.y, gp + 1);
   }
 }
 
