@@ -566,7 +566,13 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = m0 + wm + i * 16 + mfma_row(lane, r);
-        if (row < M) cb[(int64_t)row * ldc + cc] = from_f32<OutT>(acc[i][j][r] + bv);
+        if (row >= M) continue;
+        OutT* dst = cb + (int64_t)row * ldc + cc;
+        // the fp32 results that take this path (split-K partials, weight
+        // gradients in one split, a step's product for the cell kernel) are
+        // each read once: non-temporal
+        if constexpr (sizeof(OutT) == 4) __builtin_nontemporal_store(acc[i][j][r] + bv, dst);
+        else *dst = from_f32<OutT>(acc[i][j][r] + bv);
       }
   }
 }
