@@ -149,11 +149,19 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
 // lane (global_load_lds_dwordx4; lds_base is wave-uniform).  On gfx950 this
 // moves about 2.5x the bytes per CU per clock of loads into VGPRs.  The load
 // is counted by vmcnt and is invisible to the compiler's wait insertion, so
-// the caller waits explicitly (wait_vm) before the data is read.
+// the caller waits explicitly (wait_vm) before the data is read, with
+// counts that leave the later stages' loads in flight.  M0 is a reserved
+// register, which the compiler does not allocate; in the compiled kernels
+// of this library no instruction but these loads reads it (no dynamically
+// indexed register arrays, no LDS parameter loads), so the clobber only
+// documents the write and its warning is silenced.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(const void* src, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                :: "v"(src), "s"(lds_base) : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 // s_waitcnt vmcnt(N), other counters untouched.
 template <int N> __device__ __forceinline__ void wait_vm() {
