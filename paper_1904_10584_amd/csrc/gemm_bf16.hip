@@ -610,12 +610,12 @@ hipError_t launch(const GemmArgs& g, Out<OutT> dst, float* rowsum, int S, int kp
 }
 
 // The forward step with the cell in the epilogue: A = h_{t-1} [nb][H], B =
-// W_h [4H][H] read gate-interleaved, square tiles of pick_small's size.
-template <int T>
+// W_h [4H][H] read gate-interleaved, tiles of pick_small's shape.
+template <int T, int TM = T>
 hipError_t launch_cell(const GemmArgs& g, const CellArgs& cell, hipStream_t s) {
-  auto kern = gemm_bf16_kernel<true, true, float, false, false, T, T, true>;
-  constexpr int lds = Cfg<T, T>::LDS;
-  static_assert(T * (T + 4) * 4 <= lds, "the cell epilogue stages the fp32 tile in LDS");
+  auto kern = gemm_bf16_kernel<true, true, float, false, false, T, TM, true>;
+  constexpr int lds = Cfg<T, TM>::LDS;
+  static_assert(TM * (T + 4) * 4 <= lds, "the cell epilogue stages the fp32 tile in LDS");
   static bool attr = false;
   if (!attr) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -627,7 +627,7 @@ hipError_t launch_cell(const GemmArgs& g, const CellArgs& cell, hipStream_t s) {
   const bf16_t* b = static_cast<const bf16_t*>(g.B);
   Op A{a, g.lda, a, g.lda, 1 << 30};
   Op B{b, g.ldb, b, g.ldb, 1 << 30};
-  const int tm = (g.M + T - 1) / T, tn = (g.N + T - 1) / T;
+  const int tm = (g.M + TM - 1) / TM, tn = (g.N + T - 1) / T;
   Out<float> none{nullptr, 0, nullptr, 0, 1 << 30, 0};
   hipLaunchKernelGGL(kern, dim3(tm * tn), dim3(NT), lds, s, A, B, none, nullptr, nullptr, g.M,
                      g.N, g.K, g.K, tm, tn, 1, (tm <= 8 && tn >= 2 * tm ? 2 : 0), cell);
@@ -673,18 +673,22 @@ int pick_bn(int M, int N) {
 }
 
 // Products with few rows (M <= 2048, e.g. one time step of the recurrence
-// run as a product): square tiles of 128 or 64 where 256-row tiles would
-// leave most CUs idle.  Relative time = rounds of one workgroup per CU x
-// tile area / efficiency (smaller tiles read more LDS bytes per flop).
+// run as a product): tiles of 128 x 128, 64 rows x 192 columns, or 64 x 64
+// where 256-row tiles would leave most CUs idle.  Relative time = rounds of
+// one workgroup per CU x tile area / efficiency (smaller tiles read more LDS
+// bytes per flop).  Returns the tile's columns (0: the large tiles); 192
+// means 64 x 192 (e.g. B = 512 rows x 6144 columns: exactly 256 tiles,
+// where 128 x 128 tiles leave 64 CUs idle).
 int pick_small(int M, int N) {
   if (M > 2048) return 0;
   int best = 0;
   double tbest = 0.0;
-  const struct { int t; double eff; } cand[] = {{256, 1.0}, {128, 0.8}, {64, 0.55}};
+  const struct { int tm, tn; double eff; } cand[] = {
+      {256, 256, 1.0}, {128, 128, 0.8}, {64, 192, 0.8}, {64, 64, 0.55}};
   for (const auto& c : cand) {
-    const int64_t tiles = (int64_t)((M + c.t - 1) / c.t) * ((N + c.t - 1) / c.t);
-    const double t = grid_time(tiles, (double)c.t * c.t / c.eff);
-    if (best == 0 || t < tbest) { best = c.t; tbest = t; }
+    const int64_t tiles = (int64_t)((M + c.tm - 1) / c.tm) * ((N + c.tn - 1) / c.tn);
+    const double t = grid_time(tiles, (double)c.tm * c.tn / c.eff);
+    if (best == 0 || t < tbest) { best = c.tn; tbest = t; }
   }
   return best == 256 ? 0 : best;
 }
@@ -694,6 +698,7 @@ hipError_t launch_bn(int bn, const GemmArgs& g, Out<OutT> dst, float* rowsum, in
                      hipStream_t s) {
   const int sm = pick_small(g.M, g.N);
   if (sm == 128) return launch<AK, BKM, OutT, BIAS, ROWSUM, 128, 128>(g, dst, rowsum, S, kps, s);
+  if (sm == 192) return launch<AK, BKM, OutT, BIAS, ROWSUM, 192, 64>(g, dst, rowsum, S, kps, s);
   if (sm == 64) return launch<AK, BKM, OutT, BIAS, ROWSUM, 64, 64>(g, dst, rowsum, S, kps, s);
   return bn == 192 ? launch<AK, BKM, OutT, BIAS, ROWSUM, 192>(g, dst, rowsum, S, kps, s)
                    : launch<AK, BKM, OutT, BIAS, ROWSUM, 256>(g, dst, rowsum, S, kps, s);
@@ -739,7 +744,7 @@ hipError_t gemm_bf16_lstm_fwd_step(const LstmFwdStep& a, hipStream_t s, bool* do
   const int H = a.hidden;
   if (!a.bf16 || !a.hprev || a.nb <= 0 || H % 8 != 0) return hipSuccess;
   const int sm = pick_small(a.nb, 4 * H);
-  if (sm != 128 && sm != 64) return hipSuccess;
+  if (sm != 128 && sm != 192 && sm != 64) return hipSuccess;
   GemmArgs g;
   g.A = a.hprev; g.lda = H;
   g.B = a.Wh; g.ldb = H;
@@ -748,6 +753,7 @@ hipError_t gemm_bf16_lstm_fwd_step(const LstmFwdStep& a, hipStream_t s, bool* do
                       static_cast<bf16_t*>(a.H), static_cast<bf16_t*>(a.Hs), a.C,
                       static_cast<bf16_t*>(a.G), H};
   *done = true;
+  if (sm == 192) return launch_cell<192, 64>(g, cell, s);
   return sm == 128 ? launch_cell<128>(g, cell, s) : launch_cell<64>(g, cell, s);
 }
 
