@@ -10,10 +10,14 @@
 //     quarter of the MFMA peak;
 //   * a workgroup is eight waves (two per SIMD, one workgroup per CU): a
 //     single wave issues independent MFMAs at about 87 % of the peak, but
-//     four waves with 128 x 128 tiles each ran ~35 % slower than eight, not
-//     covering their LDS waits;
+//     four waves with 128 x 128 tiles each ran 25-40 % slower than eight,
+//     also with the next k-step's fragments double-buffered in registers:
+//     one wave per SIMD does not cover its own LDS waits and address work;
 //   * a 256 x BN tile (BN = 256, or 192 where that fills the CUs) with waves
-//     of 128 x BN/4 reads 384 bytes or less of LDS per MFMA.
+//     of 128 x BN/4 reads 384 bytes or less of LDS per MFMA; products of at
+//     most 2048 rows take 128 x 128, 64 x 192 or 64 x 64 tiles, whichever
+//     fills the CUs best, and one LSTM step's recurrent product can carry
+//     the cell in its epilogue (CELL).
 // Tiles keep their global layout in LDS:
 //   * a k-major tile is [rows][64 k] (128 B per row); the fragment of a
 //     16x16x32 MFMA (8 consecutive k of one row per lane) is one 16-byte LDS
