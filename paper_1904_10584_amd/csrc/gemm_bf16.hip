@@ -35,10 +35,10 @@
 // k-rows 8 apart, which the XOR alone puts on the same banks (the rotation
 // took the weight gradients' bank-conflict cycles from 15.7 % to 5.3 %).
 // This keeps the fragment reads nearly free of LDS bank conflicts and each
-// 128-byte line of a tile row in one load instruction.  Chunks outside the operand are read
-// from a zero vector.  The loads of k-tile t + NS - 1 are in flight while
-// tile t is multiplied (NS LDS stages, explicit vmcnt waits, one barrier per
-// k-tile).  Workgroups are dispatched to the 8 XCDs round-robin; the tile
+// 128-byte line of a tile row in one load instruction.  Chunks outside the
+// operand are read from a zero vector.  The loads of k-tile t + NS - 1 are
+// in flight while tile t is multiplied (NS LDS stages, explicit vmcnt waits,
+// one barrier per k-tile).  Workgroups are dispatched to the 8 XCDs round-robin; the tile
 // order gives each XCD a contiguous range of tiles, so tiles that share
 // operand rows share an L2.  Weight gradients split K over workgroups (fp32
 // partial tiles, summed in split order by splitk_reduce in gemm.hip); for an
@@ -93,7 +93,6 @@ typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
 
 // Element offset of chunk c (8 bf16) of row r in a k-major tile.
 __device__ __forceinline__ int kofs(int r, int c) { return r * BK + ((c ^ (r & 7)) << 3); }
-// Element offset of chunk c of k-row k in an m/n-major tile of R columns.
 // Slot of chunk c in k-row k of an m/n-major tile of R columns: XOR with
 // 2 (k % 4), then, where a row holds more than 8 chunks, rotated by 8 for
 // the k-rows with bit 3 set.
@@ -109,6 +108,7 @@ template <int R> __device__ __forceinline__ int mchunk(int k, int s) {
   if (NC > 8 && (k & 8)) { s -= 8; if (s < 0) s += NC; }
   return s ^ ((k & 3) << 1);
 }
+// Element offset of chunk c of k-row k in an m/n-major tile of R columns.
 template <int R> __device__ __forceinline__ int mofs(int k, int c) {
   return k * R + (mslot<R>(k, c) << 3);
 }
