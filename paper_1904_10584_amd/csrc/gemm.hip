@@ -241,6 +241,10 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(
 
 // Sum of the split-K partials in split order, routed to the two destinations,
 // and of the partial row sums.
+// V4: every destination row chunk is 16-byte aligned (pointers, pitches
+// and the column split multiples of 4 floats), so the sum leaves as one
+// 16-byte store instead of four 4-byte ones.
+template <bool V4>
 __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ part, int S, int M,
                                                      int N, float* __restrict__ c0, int64_t ld0,
                                                      float* __restrict__ c1, int64_t ld1, int split,
@@ -259,7 +263,11 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ p
     const int64_t e = i * 4;
     const int m = (int)(e / N), n = (int)(e % N);
     float* dst = n >= split ? c1 + (int64_t)m * ld1 + (n - split) : c0 + (int64_t)m * ld0 + n;
-    dst[0] = s.x; dst[1] = s.y; dst[2] = s.z; dst[3] = s.w;
+    if constexpr (V4) {
+      *reinterpret_cast<float4*>(dst) = s;
+    } else {
+      dst[0] = s.x; dst[1] = s.y; dst[2] = s.z; dst[3] = s.w;
+    }
   } else if (rowsum && i - nq < M) {
     const int64_t m = i - nq;
     float s = rs_part[m];
@@ -341,10 +349,18 @@ hipError_t splitk_reduce_launch(const float* part, int S, const GemmArgs& g, con
                                 hipStream_t s) {
   const int64_t nq = (int64_t)g.M * g.N / 4;
   const int64_t threads = nq + (g.rowsum ? g.M : 0);
-  hipLaunchKernelGGL(splitk_reduce, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, part,
-                     S, g.M, g.N, static_cast<float*>(g.C), g.ldc,
-                     static_cast<float*>(g.C2 ? g.C2 : g.C), g.C2 ? g.ldc2 : g.ldc,
-                     g.C2 ? g.n_split : (1 << 30), rs_part, g.rowsum);
+  float* c0 = static_cast<float*>(g.C);
+  float* c1 = static_cast<float*>(g.C2 ? g.C2 : g.C);
+  const int64_t ld1 = g.C2 ? g.ldc2 : g.ldc;
+  const int split = g.C2 ? g.n_split : (1 << 30);
+  const bool v4 = (reinterpret_cast<uintptr_t>(c0) | reinterpret_cast<uintptr_t>(c1)) % 16 == 0 &&
+                  g.ldc % 4 == 0 && ld1 % 4 == 0 && split % 4 == 0;
+  if (v4)
+    hipLaunchKernelGGL(splitk_reduce<true>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
+                       part, S, g.M, g.N, c0, g.ldc, c1, ld1, split, rs_part, g.rowsum);
+  else
+    hipLaunchKernelGGL(splitk_reduce<false>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
+                       part, S, g.M, g.N, c0, g.ldc, c1, ld1, split, rs_part, g.rowsum);
   return hipGetLastError();
 }
 
