@@ -219,7 +219,9 @@ def hbm_kernels(am, synth, w, n, reps):
     and r, writes r and the 2-bit codes' words (12 B per element + 4 B per
     emitted word); the decoder writes the dense update and reads the words
     (4 B per element + 4 B per word); SGD reads the master and the update
-    and writes the master and its bf16 copy (14 B per element)."""
+    and writes the master and its bf16 copy (14 B per element); the step's
+    fused decode + SGD reads the master and the words and writes the bf16
+    copy and the masters the words name (6 B per element + 8 B per word)."""
     import torch
     dev = torch.device("cuda")
     gen = torch.Generator(device=dev)
@@ -273,6 +275,10 @@ def hbm_kernels(am, synth, w, n, reps):
     master = torch.randn(n, generator=gen, device=dev) * 0.03
     wbf = torch.empty(n, dtype=torch.bfloat16, device=dev)
     out["sgd"] = dict(timed(am.K_SGD, lambda: am.sgd_apply(master, g, 1e-6, wbf)), elements=n)
+    # the step's decode + SGD pass over the same words (each word read and its
+    # element's master stored: 8 bytes per word beyond the 6 per element)
+    out["decode_sgd"] = dict(timed(am.K_SGD, lambda: am.grad_threshold_decode_sgd(words, count, tau, master, 1e-6, wbf),
+                                   count * 2), elements=n, words=int(count.item()))
     del flush
     return out
 

@@ -209,6 +209,21 @@ am_status grad_threshold_decode(const uint32_t* words, const int64_t* count, int
                                 float tau, int64_t n, float* dense, int32_t accumulate,
                                 void* stream);
 
+/* The decode of one stream (accumulate = 0) and the SGD step on its update
+ * (§VI-A decode, §VI: the update applied to the fp32 master weights) in one
+ * pass: master and weights_bf16 end up exactly as after
+ *   grad_threshold_decode(words, count, capacity, tau, n, update, 0, s);
+ *   sgd_apply(n, master, weights_bf16, update, lr, s);
+ * but the dense update is built tile by tile on chip and never stored.
+ * Elements no word names keep their master value (it is not written again
+ * when lr is +0.0 or positive and finite; see sgd_apply for the arithmetic);
+ * weights_bf16 (or NULL) is written for every element.  The same argument
+ * rules as grad_threshold_decode: words strictly ascending in index, count
+ * [device] clamped to [0, capacity], n < 2^31.                            */
+am_status grad_threshold_decode_sgd(const uint32_t* words, const int64_t* count, int64_t capacity,
+                                    float tau, int64_t n, float lr, float* master,
+                                    void* weights_bf16, void* stream);
+
 /* ---- student inputs ------------------------------------------------------ */
 
 /* Stacked frames of an utterance of raw_frames 10 ms frames: the number of

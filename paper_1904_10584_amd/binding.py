@@ -75,6 +75,7 @@ _PROTOS = {
     "grad_threshold_encode": (_I32, [_I64, _P, _P, _F32, _P, _I64, _P, _P, _I64, _P]),
     "grad_threshold_encode_noalloc": (_I32, [_I64, _P, _P, _F32, _P, _I64, _P, _P]),
     "grad_threshold_decode": (_I32, [_P, _P, _I64, _F32, _I64, _P, _I32, _P]),
+    "grad_threshold_decode_sgd": (_I32, [_P, _P, _I64, _F32, _I64, _F32, _P, _P, _P]),
     "sgd_apply": (_I32, [_I64, _P, _P, _P, _F32, _P]),
     "am_decode_multi_workspace_bytes": (_I64, [_I32, _I64]),
     "grad_threshold_decode_multi": (_I32, [_I32, _P, _I64, _P, _F32, _I64, _P, _I32, _P, _I64, _P]),
@@ -257,6 +258,15 @@ def grad_threshold_decode(words, count, tau, dense, accumulate=False, stream=Non
         _dev(words, "words", torch.int32), _dev(count, "count", torch.int64), words.numel(),
         float(tau), dense.numel(), _dev(dense, "dense", torch.float32), int(bool(accumulate)),
         _stream(stream)))
+
+
+def grad_threshold_decode_sgd(words, count, tau, master, lr, weights_bf16=None, stream=None):
+    """The decode of one stream and the SGD step on its update in one pass
+    (the dense update is not materialised)."""
+    _check(lib().grad_threshold_decode_sgd(
+        _dev(words, "words", torch.int32), _dev(count, "count", torch.int64), words.numel(),
+        float(tau), master.numel(), float(lr), _dev(master, "master", torch.float32),
+        _dev(weights_bf16, "weights_bf16", torch.bfloat16), _stream(stream)))
 
 
 def decode_multi_workspace_bytes(streams, n) -> int:

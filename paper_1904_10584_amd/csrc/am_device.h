@@ -140,6 +140,14 @@ __device__ __forceinline__ CellStep lstm_cell_step(float a0, float a1, float a2,
   return r;
 }
 
+// SGD step of one element: w <- fl32(w - lr * u) evaluated in fp64 (lr * u
+// of two fp32 values is exact in fp64, so a fused or an unfused evaluation
+// rounds identically); the bf16 copy is the round-to-nearest-even image of
+// the new fp32 value.
+__device__ __forceinline__ float sgd_one(float w, float u, double lr) {
+  return (float)((double)w - lr * (double)u);
+}
+
 // Byte address of an LDS object (for instructions that take it in M0).
 __device__ __forceinline__ uint32_t lds_address(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;

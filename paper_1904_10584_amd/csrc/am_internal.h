@@ -179,6 +179,10 @@ hipError_t gtc_encode(int64_t n, const float* g, float* r, float tau, uint32_t* 
                       int64_t* count, uint32_t* ws_mask, int32_t* ws_tile, hipStream_t s);
 hipError_t gtc_decode(const uint32_t* words, const int64_t* count, int64_t capacity, float tau,
                       int64_t n, float* dense, bool accumulate, hipStream_t s);
+// Decode of one stream (accumulate = 0) fused with sgd_apply: the same
+// master and bf16 copy bit for bit, without the dense update.
+hipError_t gtc_decode_sgd(const uint32_t* words, const int64_t* count, int64_t capacity, float tau,
+                          int64_t n, float lr, float* master, uint16_t* w_bf16, hipStream_t s);
 // Aggregate of `streams` workers' streams, words [streams][capacity];
 // ws_start holds streams x (gtc_tiles(n) + 1) int32.
 hipError_t gtc_decode_multi(int streams, const uint32_t* words, int64_t capacity,

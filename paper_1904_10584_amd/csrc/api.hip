@@ -684,6 +684,21 @@ am_status grad_threshold_decode(const uint32_t* words, const int64_t* count, int
   return hip_check(am::gtc_decode(words, count, capacity, tau, n, dense, accumulate != 0, s), "decode");
 }
 
+am_status grad_threshold_decode_sgd(const uint32_t* words, const int64_t* count, int64_t capacity,
+                                    float tau, int64_t n, float lr, float* master,
+                                    void* weights_bf16, void* stream) {
+  if (n < 0 || n >= (1ll << 31)) return fail(AM_EINVAL, "n outside [0, 2^31)");
+  if (capacity < 0) return fail(AM_EINVAL, "capacity < 0");
+  if (!count || (n > 0 && !master) || (capacity > 0 && !words)) return fail(AM_EINVAL, "NULL pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // bytes: the master read, the bf16 copy written (the words and the few
+  // masters stored again are not counted)
+  Timed tm(AM_K_SGD, s, 2.0 * n, (weights_bf16 ? 6.0 : 4.0) * n);
+  return hip_check(am::gtc_decode_sgd(words, count, capacity, tau, n, lr, master,
+                                      static_cast<uint16_t*>(weights_bf16), s),
+                   "decode + sgd");
+}
+
 int64_t am_decode_multi_workspace_bytes(int32_t streams, int64_t n) {
   if (streams < 0 || n < 0) return -1;
   return align256((int64_t)streams * (am::gtc_tiles(n) + 1) * 4);

@@ -270,6 +270,68 @@ __global__ __launch_bounds__(TPB) void gtc_decode_tiles(const uint32_t* __restri
 }
 
 
+// Decode of one stream fused with the SGD step: each tile's update is built
+// in LDS as in gtc_decode_tiles (accumulate = 0) and applied to the master
+// weights at once, so the dense update never goes to memory.  An element no
+// word names has update +0.0, and fl32(w - lr * 0.0) = w for every non-NaN w
+// when lr is +0.0 or positive and finite (SKIP): its master is then not
+// stored again; the bf16 copy is written for every element, as sgd_apply
+// does.  Same results as the two launches, bit for bit.
+template <bool ALIGNED, bool BF16>
+__global__ __launch_bounds__(TPB) void gtc_decode_sgd_tiles(
+    const uint32_t* __restrict__ words, const int64_t* __restrict__ count, int64_t capacity,
+    float tau, int64_t n, float lr, bool skip, float* __restrict__ master, bf16_t* __restrict__ wb) {
+  __shared__ float tile[TILE];
+  __shared__ int64_t range[2];
+  const int64_t base = (int64_t)blockIdx.x * TILE;
+  const int64_t len = n - base < TILE ? n - base : TILE;
+  if (threadIdx.x < 128) {  // wave 0: the tile's first word, wave 1: the next tile's
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    int64_t cnt = *count;
+    cnt = cnt < 0 ? 0 : (cnt > capacity ? capacity : cnt);
+    const int64_t end = base + (wv ? len : 0);
+    const int64_t r = lower_bound_wave(words, cnt, (uint32_t)(end << 1), lane);
+    if (lane == 0) range[wv] = r;
+  }
+  for (int i = threadIdx.x; i < TILE; i += TPB) tile[i] = 0.f;
+  __syncthreads();
+  const int64_t lo = range[0], hi = range[1];
+  for (int64_t w = lo + threadIdx.x; w < hi; w += TPB) {
+    const uint32_t word = words[w];
+    const int i = (int)((word >> 1) - (uint32_t)base);
+    if ((unsigned)i >= (unsigned)len) continue;  // only for unsorted input
+    tile[i] = (word & 1u) ? -tau : tau;
+  }
+  __syncthreads();
+  const double lr64 = (double)lr;
+  // stored again: any update bit set (including -0.0), a NaN, or no SKIP
+  auto keep = [&](float m, float u) { return skip && __float_as_uint(u) == 0u && m == m; };
+  for (int i = threadIdx.x * 4; i < len; i += TPB * 4) {
+    float* mp = master + base + i;
+    if (ALIGNED && i + 3 < len) {
+      const float4 m = *reinterpret_cast<const float4*>(mp);
+      const float4 u = *reinterpret_cast<const float4*>(tile + i);
+      const float4 w = make_float4(sgd_one(m.x, u.x, lr64), sgd_one(m.y, u.y, lr64),
+                                   sgd_one(m.z, u.z, lr64), sgd_one(m.w, u.w, lr64));
+      if (!(keep(m.x, u.x) && keep(m.y, u.y) && keep(m.z, u.z) && keep(m.w, u.w)))
+        *reinterpret_cast<float4*>(mp) = w;
+      if (BF16) {
+        uint2 b;
+        b.x = (uint32_t)f32_to_bf16(w.x) | ((uint32_t)f32_to_bf16(w.y) << 16);
+        b.y = (uint32_t)f32_to_bf16(w.z) | ((uint32_t)f32_to_bf16(w.w) << 16);
+        *reinterpret_cast<uint2*>(wb + base + i) = b;
+      }
+    } else {
+      for (int k = 0; k < 4 && i + k < len; ++k) {
+        const float m = mp[k], u = tile[i + k];
+        const float w = sgd_one(m, u, lr64);
+        if (!keep(m, u)) mp[k] = w;
+        if (BF16) wb[base + i + k] = f32_to_bf16(w);
+      }
+    }
+  }
+}
+
 // ---- aggregate of several workers' streams ----------------------------------
 // Streams are the rows of words [S][capacity], each ascending in index.  A
 // bounds pass finds, for every stream s and tile t, the first word of s at or
@@ -396,6 +458,27 @@ hipError_t gtc_decode_multi(int streams, const uint32_t* words, int64_t capacity
   else
     hipLaunchKernelGGL(gtc_multi_tiles<false>, dim3((unsigned)ntiles), dim3(TPB), 0, s, words,
                        capacity, counts, streams, ws_start, ntiles, tau, n, dense);
+  return hipGetLastError();
+}
+
+hipError_t gtc_decode_sgd(const uint32_t* words, const int64_t* count, int64_t capacity, float tau,
+                          int64_t n, float lr, float* master, uint16_t* w_bf16, hipStream_t s) {
+  const int64_t ntiles = gtc_tiles(n);
+  if (ntiles == 0) return hipSuccess;
+  const bool al = (reinterpret_cast<uintptr_t>(master) & 15) == 0 &&
+                  (reinterpret_cast<uintptr_t>(w_bf16) & 7) == 0;
+  const uint32_t lb = __builtin_bit_cast(uint32_t, lr);
+  const bool skip = lb == 0u || (lr > 0.f && lr <= 3.402823466e38f);
+  bf16_t* wb = reinterpret_cast<bf16_t*>(w_bf16);
+  const dim3 g((unsigned)ntiles), b(TPB);
+  if (al && wb)
+    hipLaunchKernelGGL((gtc_decode_sgd_tiles<true, true>), g, b, 0, s, words, count, capacity, tau, n, lr, skip, master, wb);
+  else if (al)
+    hipLaunchKernelGGL((gtc_decode_sgd_tiles<true, false>), g, b, 0, s, words, count, capacity, tau, n, lr, skip, master, wb);
+  else if (wb)
+    hipLaunchKernelGGL((gtc_decode_sgd_tiles<false, true>), g, b, 0, s, words, count, capacity, tau, n, lr, skip, master, wb);
+  else
+    hipLaunchKernelGGL((gtc_decode_sgd_tiles<false, false>), g, b, 0, s, words, count, capacity, tau, n, lr, skip, master, wb);
   return hipGetLastError();
 }
 

@@ -9,12 +9,8 @@
 namespace am {
 namespace {
 
-// w <- fl32(w - lr * u) evaluated in fp64 (lr * u of two fp32 values is exact
-// in fp64, so a fused or an unfused evaluation rounds identically); the bf16
-// copy is the round-to-nearest-even image of the new fp32 value.
-__device__ __forceinline__ float sgd_one(float w, float u, double lr) {
-  return (float)((double)w - lr * (double)u);
-}
+// (sgd_one, the step of one element, is in am_device.h: the fused decode +
+// SGD of gtc.hip applies the same arithmetic.)
 
 template <bool ALIGNED, bool BF16>
 __global__ __launch_bounds__(256) void sgd_kernel(int64_t n, float* __restrict__ master,

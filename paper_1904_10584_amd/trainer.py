@@ -3,7 +3,8 @@
 forward (lstm_am_forward) -> loss and logit gradient (sparse_soft_ce) ->
 BPTT (lstm_am_backward) -> [threshold encode of the gradient with residual
 error feedback -> decode] -> SGD on the fp32 master weights with a fresh bf16
-copy.  Every step runs on the current HIP stream without host
+copy (with threshold compression, decode and SGD run as one pass:
+grad_threshold_decode_sgd).  Every step runs on the current HIP stream without host
 synchronisation; this module only owns buffers and orders the calls.
 
 A recurrence whose step barrier timed out (its workgroups were not all
@@ -34,7 +35,6 @@ class StudentStep:
         self.weights = torch.zeros(self.n, dtype=torch.bfloat16, device=dev) if self.bf16 else None
         self.grads = torch.zeros(self.n, dtype=f32, device=dev)
         self.residual = torch.zeros(self.n, dtype=f32, device=dev)
-        self.update = torch.zeros(self.n, dtype=f32, device=dev)
         self.words = torch.zeros(self.n, dtype=torch.int32, device=dev)
         self.count = torch.zeros(1, dtype=torch.int64, device=dev)
         self.x = torch.zeros((self.N, model.input_dim), dtype=model.torch_dtype, device=dev)
@@ -82,11 +82,11 @@ class StudentStep:
         if self.gtc:
             am.grad_threshold_encode(self.grads, self.residual, self.tau, self.words, self.count,
                                      self.enc_ws)
-            am.grad_threshold_decode(self.words, self.count, self.tau, self.update)
-            upd = self.update
+            # decode + SGD in one pass (the same bits as the two calls)
+            am.grad_threshold_decode_sgd(self.words, self.count, self.tau, self.master, self.lr,
+                                         self.weights)
         else:
-            upd = self.grads
-        am.sgd_apply(self.master, upd, self.lr, self.weights)
+            am.sgd_apply(self.master, self.grads, self.lr, self.weights)
 
     def check(self):
         """Synchronise; raise if a recurrence step barrier of the last pass

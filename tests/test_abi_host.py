@@ -119,6 +119,17 @@ def test_encode_decode_ce_sgd_argument_checks(L):
     assert st == -1
     st, _ = _status(L, "sgd_apply", -1, fake, None, fake, ctypes.c_float(0.1), None)
     assert st == -1
+    f = ctypes.c_float
+    st, _ = _status(L, "grad_threshold_decode_sgd", fake, fake, 10, f(1e-3), 1 << 31, f(0.1), fake, None, None)
+    assert st == -1   # n outside [0, 2^31)
+    st, _ = _status(L, "grad_threshold_decode_sgd", fake, fake, -1, f(1e-3), n, f(0.1), fake, None, None)
+    assert st == -1   # negative capacity
+    st, _ = _status(L, "grad_threshold_decode_sgd", fake, None, 10, f(1e-3), n, f(0.1), fake, None, None)
+    assert st == -1   # no count
+    st, _ = _status(L, "grad_threshold_decode_sgd", fake, fake, 10, f(1e-3), n, f(0.1), None, None, None)
+    assert st == -1   # no master
+    st, _ = _status(L, "grad_threshold_decode_sgd", None, fake, 10, f(1e-3), n, f(0.1), fake, None, None)
+    assert st == -1   # words missing for a positive capacity
     for s in (0, -1, -2, -3, -4, -5, -6):
         assert L.am_status_string(s)
     assert b"timed out" in L.am_status_string(-6)

@@ -152,6 +152,66 @@ def test_decode_bit_exact(n, accumulate):
     np.testing.assert_array_equal(_bits32(dense.cpu().numpy()), _bits32(ref))
 
 
+@pytest.mark.parametrize("n,offset", [(1, 0), (4097, 1), (1_000_003, 0)])
+@pytest.mark.parametrize("lr", [0.01, 0.0, -0.0, -0.5, float("nan"), float("inf")])
+@pytest.mark.parametrize("with_bf16", [True, False])
+def test_decode_sgd_matches_decode_then_sgd(n, offset, lr, with_bf16):
+    """The fused pass against the two calls on the GPU (bit for bit, master
+    values with NaNs and signed zeros; the learning rates that are not +0.0
+    or positive and finite turn off its skipping of unnamed elements) and,
+    for finite values, against the oracle's decode followed by its SGD."""
+    say(f"decode+sgd n={n} offset={offset} lr={lr} bf16={with_bf16}")
+    rng = np.random.default_rng(n + offset)
+    tau = np.float32(1e-3)
+    g = (rng.standard_normal(n) * 1.5e-3).astype(np.float32)
+    _, ref_w, ref_c = oracle.grad_threshold_encode(g, np.zeros(n, np.float32), tau)
+    _, _, c, words, count = _encode_gpu(g, np.zeros(n, np.float32), tau)
+    m0 = rng.standard_normal(n + offset).astype(np.float32)
+    special = np.array([0.0, -0.0, 1e-40, -3e38, np.nan], np.float32)
+    m0[offset:offset + min(5, n)] = special[:min(5, n)]
+    lr32 = np.float32(lr)
+    fused = to_dev(m0)
+    two = to_dev(m0)
+    fb = torch.zeros(n + offset, dtype=torch.bfloat16, device="cuda") if with_bf16 else None
+    tb = torch.zeros(n + offset, dtype=torch.bfloat16, device="cuda") if with_bf16 else None
+    am.grad_threshold_decode_sgd(words, count, tau, fused[offset:], lr32,
+                                 fb[offset:] if with_bf16 else None)
+    dense = torch.full((n,), 7.0, dtype=torch.float32, device="cuda")
+    am.grad_threshold_decode(words, count, tau, dense)
+    am.sgd_apply(two[offset:], dense, lr32, tb[offset:] if with_bf16 else None)
+    np.testing.assert_array_equal(_bits32(fused.cpu().numpy()), _bits32(two.cpu().numpy()))
+    if with_bf16:
+        np.testing.assert_array_equal(fb.cpu().view(torch.int16).numpy(), tb.cpu().view(torch.int16).numpy())
+    if np.isfinite(lr32):
+        finite = np.isfinite(m0[offset:])
+        u = oracle.grad_threshold_decode(ref_w, ref_c, tau, n)
+        ref_m, ref_b = oracle.sgd_apply(m0[offset:], u, lr32)
+        got = fused.cpu().numpy()[offset:]
+        np.testing.assert_array_equal(_bits32(got[finite]), _bits32(ref_m[finite]))
+        if with_bf16:
+            got_b = fb.cpu().view(torch.int16).numpy().view(np.uint16)[offset:]
+            np.testing.assert_array_equal(got_b[finite], ref_b[finite])
+
+
+def test_decode_sgd_count_clamped_to_capacity():
+    """A device count above the words' capacity is clamped, as in decode."""
+    n = 50_000
+    rng = np.random.default_rng(3)
+    tau = np.float32(1e-3)
+    g = (rng.standard_normal(n) * 1.5e-3).astype(np.float32)
+    _, _, c, words, count = _encode_gpu(g, np.zeros(n, np.float32), tau)
+    cap = max(1, c // 2)
+    part = words[:cap].clone()
+    big = torch.tensor([c + 1000], dtype=torch.int64, device="cuda")
+    m0 = rng.standard_normal(n).astype(np.float32)
+    fused, two = to_dev(m0), to_dev(m0)
+    am.grad_threshold_decode_sgd(part, big, tau, fused, 0.01)
+    dense = torch.zeros(n, dtype=torch.float32, device="cuda")
+    am.grad_threshold_decode(part, big, tau, dense)
+    am.sgd_apply(two, dense, 0.01)
+    np.testing.assert_array_equal(_bits32(fused.cpu().numpy()), _bits32(two.cpu().numpy()))
+
+
 def _ce_case(N, C, K, seed, empty_slots=False, dup=False, mask=False):
     rng = np.random.default_rng(seed)
     z = (rng.standard_normal((N, C)) * 3).astype(np.float32)

@@ -166,8 +166,9 @@ def test_threshold_compression_100_steps_bit_exact():
         np.testing.assert_array_equal(st.residual.cpu().numpy().view(np.uint32), r_ref.view(np.uint32))
         np.testing.assert_array_equal(st.words[:c].cpu().numpy().view(np.uint32), w_ref)
         if check_sgd:
+            # the step applies decode and SGD as one pass; its master and
+            # bf16 copy against the oracle's decode followed by its SGD
             u = oracle.grad_threshold_decode(w_ref, c_ref, tau, st.n)
-            np.testing.assert_array_equal(st.update.cpu().numpy().view(np.uint32), u.view(np.uint32))
             new_master, new_bits = oracle.sgd_apply(master_before, u, w["lr"])
             np.testing.assert_array_equal(st.master.cpu().numpy().view(np.uint32),
                                           new_master.view(np.uint32))
