@@ -177,6 +177,15 @@ template <int N> __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// The same wait as an opaque instruction, for counts that include loads the
+// compiler issued itself: it neither drops nor merges the wait (its own
+// bookkeeping may find such a count already met), and it still places its
+// own waits before the first use of each of those loads.
+template <int N> __device__ __forceinline__ void wait_vm_asm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

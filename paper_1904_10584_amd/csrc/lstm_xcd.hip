@@ -269,14 +269,20 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
     nb = active_down(ps, nb, t);
     if (b0 >= nb) break;  // this block of sequences has ended for good
 
-    // input projections of this lane's cells (independent of the exchange;
-    // clamped, unmasked loads so that they issue back to back)
+    // Input projections of this lane's cells (independent of the exchange;
+    // clamped, unmasked loads so that they issue back to back).  Waves 1-7
+    // issue them before the exchange, so that they have the poll's time to
+    // arrive; the polling wave issues its own after the poll, which would
+    // otherwise wait for them (its memory counter retires in order).
     bf16_t pin[FIN][4];
-    const bf16_t* prow = P + (int64_t)(off + min(b0 + qrow, nb - 1)) * G4;
+    auto load_pin = [&]() {
+      const bf16_t* prow = P + (int64_t)(off + min(b0 + qrow, nb - 1)) * G4;
 #pragma unroll
-    for (int o = 0; o < FIN; ++o)
+      for (int o = 0; o < FIN; ++o)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) pin[o][q] = prow[q * H + unit(o)];
+        for (int q = 0; q < 4; ++q) pin[o][q] = prow[q * H + unit(o)];
+    };
+    if (wave != 0) load_pin();
 
     f32x4_t acc[TPW];
 #pragma unroll
@@ -290,6 +296,7 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
       post_stores(drow, dc, dg, dh);
       drow = -1;
     }
+    if (wave == 0) load_pin();
     if (hsrc) {
       // the block's rows of h_{t-1} (inactive rows read an active one) to
       // LDS, by waves 1-7
@@ -523,14 +530,19 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
     const int nb_prev = t > 0 ? active_up(ps, nb, t - 1) : 0;
     const int off_prev = off - nb_prev;
 
-    // this wave's cell inputs (independent of the exchange)
+    // This wave's cell inputs (independent of the exchange), issued after
+    // the first two chunks' direct loads so that the chunk waits can leave
+    // them in flight: NL loads, the same number in every wave (clamped
+    // addresses for items past the wave's last), which the wait counts below
+    // assume.  Issued before the exchange instead, they would sit ahead of
+    // the chunks in the in-order memory counter and hold up the product.
     bf16_t gv[IPS][4], dhv[IPS];
     float cv[IPS], cpv[IPS];
-    {
+    constexpr int NL = 4 * IPS;  // gates (8 bytes), c_t, c_{t-1}, dh_t per item
+    auto load_cell = [&]() {
       const float* cprev_rows = t > 0 ? a.C + (int64_t)off_prev * H : a.c0;
 #pragma unroll
       for (int k = 0; k < IPS; ++k) {
-        if (k >= nitems) break;  // (wave-uniform)
         const int b = min(b0 + item_row(k), nb - 1), j = item_j(k);
         const int64_t o = (int64_t)(off + b) * H + j;
         load_gates(Gb + (int64_t)(off + b) * G4, j, gv[k]);
@@ -538,7 +550,7 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
         cpv[k] = cprev_rows[(int64_t)b * H + j];
         dhv[k] = dHa[o];
       }
-    }
+    };
 
     f32x4_t acc[MT][NTU];
 #pragma unroll
@@ -562,10 +574,19 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
       };
       issue(0, 0);
       if (NCH > 1) issue(1, 1);
+      load_cell();
+      // in flight after chunk c: chunk c + 1 (when issued) and the cell
+      // loads while c is one of the first two chunks
+      constexpr int CP = NCH > 1 ? 1 : 0;
 #pragma unroll
       for (int c = 0; c < NCH; ++c) {
-        if (c + 1 < NCH) wait_vm<IPC>();
-        else wait_vm<0>();
+        if (c + 1 < NCH) {
+          if (c <= CP) wait_vm_asm<IPC + NL>();
+          else wait_vm_asm<IPC>();
+        } else {
+          if (c <= CP) wait_vm_asm<NL>();
+          else wait_vm_asm<0>();
+        }
         const bf16_t* bb = buf + (c & 1) * (CHB / 2);
 #pragma unroll
         for (int ks = 0; ks < CH; ++ks) {
@@ -585,6 +606,8 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
           issue(c + 2, c & 1);
         }
       }
+    } else {
+      load_cell();
     }
     // fixed-order sum of the eight partial products
     __syncthreads();
