@@ -186,6 +186,18 @@ template <int N> __device__ __forceinline__ void wait_vm_asm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// wait_vm_asm<n> for a count n that is a constant once the caller's loops
+// are unrolled (the chain folds to one instruction); a count above N, or
+// one left unresolved, waits for every load (vmcnt 0).
+template <int N> __device__ __forceinline__ void wait_vm_n(int n) {
+  if constexpr (N == 0) {
+    wait_vm_asm<0>();
+  } else {
+    if (n == N) wait_vm_asm<N>();
+    else wait_vm_n<N - 1>(n);
+  }
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

@@ -439,24 +439,33 @@ __global__ __launch_bounds__(512, 1) void lstm_fwd_xcd(PersistFwd a, PersistSche
 // range: wave w multiplies k-steps [w KW, (w+1) KW) and keeps the W_h^T
 // fragments of those k-steps, for every unit tile, in registers.  Each wave
 // fetches its k-slice of the block's dA_{t+1} rows itself, with direct loads
-// into two private LDS buffers in chunks of CH k-steps, so it waits only on
-// its own loads.  The eight partial products are summed in a fixed order
-// through LDS; the cell backward (dc carried in registers) is spread over
-// the first seven waves in items of one row per lane, an equal number per
-// SIMD, while the last wave polls the step barrier.
+// into private LDS buffers in chunks of CH k-steps, so it waits only on its
+// own loads: one buffer per chunk where the LDS holds them all (16-row
+// blocks: three chunks, 96 KiB over the eight waves), else two used in turn.
+// The eight partial products are summed in a fixed order through LDS; the
+// cell backward (dc carried in registers) is spread over the first seven
+// waves in items of one row per lane, an equal number per SIMD, while the
+// last wave polls the step barrier.
+constexpr int bwd_chunk_buffers(int MT, int KW) {
+  const int ch = KW >= 4 ? 4 : KW, nch = KW / ch;
+  const int fit = 160 * 1024 / (8 * 16 * MT * ch * 64);  // buffer sets the LDS holds
+  return nch < fit ? nch : (fit < 2 ? fit : 2);
+}
 template <int MT, int NTU, int KW>
 __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSchedule ps, XcdSync y) {
   constexpr int RB = 16 * MT;                 // sequences per block
   constexpr int CH = KW >= 4 ? 4 : KW;        // k-steps per chunk
   constexpr int NCH = KW / CH;                // chunks per step
+  constexpr int NB = bwd_chunk_buffers(MT, KW);  // chunk buffers per wave
   constexpr int CPR = CH * 4;                 // 16-byte pieces per chunk row
   constexpr int SW = (CPR < 8 ? CPR : 8) - 1; // swizzle mask
   constexpr int CHB = RB * CH * 64;           // bytes per chunk
   constexpr int IPC = CHB / 1024;             // direct loads per chunk
   static_assert(KW % CH == 0 && IPC >= 1, "chunking");
+  static_assert(NB >= 1 && NB <= NCH, "chunk buffers");
   static_assert(MT * NTU * 4 <= 32, "cell items: at most 8 per SIMD");
   extern __shared__ __align__(16) unsigned char lds[];
-  bf16_t* buf = reinterpret_cast<bf16_t*>(lds + (threadIdx.x >> 6) * 2 * CHB);
+  bf16_t* buf = reinterpret_cast<bf16_t*>(lds + (threadIdx.x >> 6) * NB * CHB);
   f32x4_t* red = reinterpret_cast<f32x4_t*>(lds);  // [8][MT][NTU][64], after the products
   __shared__ int bad_sh;
 
@@ -572,22 +581,20 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
                 __builtin_amdgcn_readfirstlane(lds_address(buf + bi * (CHB / 2) + i * 512)));
         }
       };
-      issue(0, 0);
-      if (NCH > 1) issue(1, 1);
+      // the first NB chunks at once (every chunk where the buffers allow:
+      // one memory latency per step rather than one per buffer round), then
+      // the cell inputs; chunk c + NB goes into chunk c's buffer once c has
+      // been read
+#pragma unroll
+      for (int c = 0; c < NB; ++c) issue(c, c);
       load_cell();
-      // in flight after chunk c: chunk c + 1 (when issued) and the cell
-      // loads while c is one of the first two chunks
-      constexpr int CP = NCH > 1 ? 1 : 0;
 #pragma unroll
       for (int c = 0; c < NCH; ++c) {
-        if (c + 1 < NCH) {
-          if (c <= CP) wait_vm_asm<IPC + NL>();
-          else wait_vm_asm<IPC>();
-        } else {
-          if (c <= CP) wait_vm_asm<NL>();
-          else wait_vm_asm<0>();
-        }
-        const bf16_t* bb = buf + (c & 1) * (CHB / 2);
+        // in flight behind chunk c at its wait: the chunks issued after it
+        // (up to c + NB - 1) and, while c is one of the first NB, the cell
+        // loads
+        wait_vm_n<40>(((c + NB < NCH ? c + NB : NCH) - c - 1) * IPC + (c < NB ? NL : 0));
+        const bf16_t* bb = buf + (c % NB) * (CHB / 2);
 #pragma unroll
         for (int ks = 0; ks < CH; ++ks) {
           Frag<bf16_t> af[MT];
@@ -601,9 +608,9 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
 #pragma unroll
             for (int m = 0; m < MT; ++m) mma_16x16x32(acc[m][n], af[m], wb[c * CH + ks][n]);
         }
-        if (c + 2 < NCH) {
+        if (c + NB < NCH) {
           __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this buffer's reads are done
-          issue(c + 2, c & 1);
+          issue(c + NB, c % NB);
         }
       }
     } else {
@@ -757,9 +764,9 @@ hipError_t lstm_bwd_xcd_launch(PersistBwd a, PersistSchedule ps, XcdSync y, hipS
   y.units = x.U;
   y.fenced = fenced_forced() ? 1 : 0;
   const int blocks = NX * x.BPX * (a.hidden / x.U);
-  // two private chunk buffers per wave, or the partial products if larger
+  // the waves' private chunk buffers, or the partial products if larger
   const int ch = x.KW >= 4 ? 4 : x.KW;
-  const size_t chunks = (size_t)8 * 2 * 16 * x.MT * ch * 64;
+  const size_t chunks = (size_t)8 * bwd_chunk_buffers(x.MT, x.KW) * 16 * x.MT * ch * 64;
   const size_t red = (size_t)8 * x.MT * x.NTU * 64 * 16;
   const size_t lds = chunks > red ? chunks : red;
   void* args[] = {&a, &ps, &y};
