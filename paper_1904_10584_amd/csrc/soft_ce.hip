@@ -5,9 +5,9 @@
 // issued back to back and kept in registers (up to 8192 classes), max and
 // sum-of-exponentials are
 // wave reductions, the k teacher logits are read with wave-uniform loads, and
-// the gradient row  s (M softmax(z) - scatter(p))  is written once.  A teacher
-// entry is subtracted by the one lane that holds its class; which register
-// holds it is a wave-uniform choice, taken with uniform branches.  Row losses
+// the gradient row  s (M softmax(z) - scatter(p))  is written once.  The
+// teacher terms reach the lanes that hold their classes through a small LDS
+// scratch per wave (one 256-class chunk at a time).  Row losses
 // are summed per block in a fixed order, then over blocks by a single block,
 // so the loss is deterministic.
 #include "am_device.h"
@@ -36,6 +36,7 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
     const float* __restrict__ scale_dev, float scale_host, DT* __restrict__ dz,
     float* __restrict__ partials) {
   __shared__ float wl[ROWS_PER_BLOCK];
+  __shared__ __align__(16) float corr[ROWS_PER_BLOCK][256];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t f = (int64_t)blockIdx.x * ROWS_PER_BLOCK + wave;
   float row_loss = 0.f;
@@ -123,17 +124,39 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
         v[i].z *= sm;
         v[i].w *= sm;
       }
-      for (int jj = 0; jj < K; ++jj) {
-        int c;
-        float p;
-        if (jj < 64) {  // broadcast entry jj from the lane that loaded it
-          c = __builtin_amdgcn_readlane(tc, jj);
-          p = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, tp), jj));
-        } else {
-          c = ir[jj];
-          p = pr[jj];
-          if (c >= C) c = -1;
+      // Entries 0-63 (one per lane): s p_j comes off the slot of class c_j
+      // through a 1 KiB LDS scratch of the wave, one 256-class chunk at a
+      // time: zeroed, each entry lane adds its term at its class (an LDS
+      // atomic add, so that repeated classes sum), every lane reads its four
+      // slots back.  A wave's LDS operations run in order, so no barrier is
+      // needed; the chunks' operations issue back to back.
+      {
+        float* cw = corr[wave];
+        const float dj = tc >= 0 ? s * tp : 0.f;
+        const int tch = tc >= 0 ? tc >> 8 : -1, tslot = tc & 255;
+        float4 cv[NCH];
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+          reinterpret_cast<float4*>(cw)[lane] = make_float4(0.f, 0.f, 0.f, 0.f);
+          __builtin_amdgcn_wave_barrier();
+          if (tch == i) atomicAdd(cw + tslot, dj);
+          __builtin_amdgcn_wave_barrier();
+          cv[i] = reinterpret_cast<const float4*>(cw)[lane];
+          __builtin_amdgcn_wave_barrier();
         }
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+          v[i].x -= cv[i].x;
+          v[i].y -= cv[i].y;
+          v[i].z -= cv[i].z;
+          v[i].w -= cv[i].w;
+        }
+      }
+      // entries past the 64th (K > 64), one at a time
+      for (int jj = 64; jj < K; ++jj) {
+        int c = ir[jj];
+        const float p = pr[jj];
+        if (c >= C) c = -1;
         if (c < 0) continue;
         const int owner = (c & 255) >> 2, cc = c & 3;
         const float d = lane == owner ? s * p : 0.f;
