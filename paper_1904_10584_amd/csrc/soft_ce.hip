@@ -192,12 +192,25 @@ __global__ __launch_bounds__(256) void soft_ce_rows(
   if (threadIdx.x == 0) partials[blockIdx.x] = ((wl[0] + wl[1]) + wl[2]) + wl[3];
 }
 
-// Fixed-order sum of the per-block losses.
+// Fixed-order sum of the per-block losses: thread x adds elements x, x + 256,
+// ... in that order, then a tree over the threads.  The loads of a batch of
+// 16 are issued before its adds, so that a thread waits for memory once per
+// batch rather than once per element.
 __global__ __launch_bounds__(256) void sum_partials(const float* __restrict__ partials, int64_t n,
                                                     float* __restrict__ out) {
   __shared__ float red[256];
   float acc = 0.f;
-  for (int64_t i = threadIdx.x; i < n; i += 256) acc += partials[i];
+  for (int64_t b = 0; b < n; b += 16 * 256) {
+    float v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int64_t i = b + (int64_t)k * 256 + threadIdx.x;
+      v[k] = i < n ? partials[i] : 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      if (b + (int64_t)k * 256 + threadIdx.x < n) acc += v[k];
+  }
   red[threadIdx.x] = acc;
   __syncthreads();
   for (int o = 128; o > 0; o >>= 1) {
