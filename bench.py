@@ -228,8 +228,8 @@ def hbm_kernels(am, synth, w, n, reps):
     gen.manual_seed(8)
     flush = torch.zeros(1 << 28, device=dev)  # 1 GiB
 
-    def timed(cls, launch, count=None):
-        # count: device word count of each launch (4 bytes per word are
+    def timed(cls, launch, count=None, word_bytes=4.0):
+        # count: device word count of each launch (word_bytes per word are
         # added to the library's per-element bytes), summed on the device
         res = {}
         for mode in ("in_loop", "flushed"):
@@ -246,7 +246,7 @@ def hbm_kernels(am, synth, w, n, reps):
                     words += count
             am.profile_end()
             kt = am.profile_get(cls)
-            res[mode] = _hbm_entry(dict(kt, bytes=kt["bytes"] + 4.0 * float(words.item())), reps)
+            res[mode] = _hbm_entry(dict(kt, bytes=kt["bytes"] + word_bytes * float(words.item())), reps)
         return res
 
     out = {}
@@ -275,10 +275,11 @@ def hbm_kernels(am, synth, w, n, reps):
     master = torch.randn(n, generator=gen, device=dev) * 0.03
     wbf = torch.empty(n, dtype=torch.bfloat16, device=dev)
     out["sgd"] = dict(timed(am.K_SGD, lambda: am.sgd_apply(master, g, 1e-6, wbf)), elements=n)
-    # the step's decode + SGD pass over the same words (each word read and its
-    # element's master stored: 8 bytes per word beyond the 6 per element)
+    # the step's decode + SGD pass over the same words: with a positive
+    # learning rate only the named elements are touched, 14 bytes per word
+    # (the word, the master read and stored, its bf16 copy)
     out["decode_sgd"] = dict(timed(am.K_SGD, lambda: am.grad_threshold_decode_sgd(words, count, tau, master, 1e-6, wbf),
-                                   count * 2), elements=n, words=int(count.item()))
+                                   count, 14.0), elements=n, words=int(count.item()))
     del flush
     return out
 

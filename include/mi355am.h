@@ -214,12 +214,17 @@ am_status grad_threshold_decode(const uint32_t* words, const int64_t* count, int
  * pass: master and weights_bf16 end up exactly as after
  *   grad_threshold_decode(words, count, capacity, tau, n, update, 0, s);
  *   sgd_apply(n, master, weights_bf16, update, lr, s);
- * but the dense update is built tile by tile on chip and never stored.
- * Elements no word names keep their master value (it is not written again
- * when lr is +0.0 or positive and finite; see sgd_apply for the arithmetic);
- * weights_bf16 (or NULL) is written for every element.  The same argument
- * rules as grad_threshold_decode: words strictly ascending in index, count
- * [device] clamped to [0, capacity], n < 2^31.                            */
+ * provided that, when lr is +0.0 or positive and finite, weights_bf16 (if
+ * given) holds the round-to-nearest-even bf16 rounding of master at every
+ * element no word names, and no such master is NaN.  sgd_apply and this
+ * call leave the copy in that state.  With such an lr only the named
+ * elements are read and written (an unnamed element's update is +0.0, and
+ * w - lr * 0.0 = w), so the pass costs about 14 bytes per word rather than
+ * a pass over all n; every other master and bf16 value is left as it is.
+ * With any other lr (-0.0, negative, infinite, NaN) every element is
+ * rewritten.  See sgd_apply for the arithmetic.  The same argument rules as
+ * grad_threshold_decode: words strictly ascending in index, count [device]
+ * clamped to [0, capacity], n < 2^31.                                     */
 am_status grad_threshold_decode_sgd(const uint32_t* words, const int64_t* count, int64_t capacity,
                                     float tau, int64_t n, float lr, float* master,
                                     void* weights_bf16, void* stream);

@@ -691,9 +691,13 @@ am_status grad_threshold_decode_sgd(const uint32_t* words, const int64_t* count,
   if (capacity < 0) return fail(AM_EINVAL, "capacity < 0");
   if (!count || (n > 0 && !master) || (capacity > 0 && !words)) return fail(AM_EINVAL, "NULL pointer");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  // bytes: the master read, the bf16 copy written (the words and the few
-  // masters stored again are not counted)
-  Timed tm(AM_K_SGD, s, 2.0 * n, (weights_bf16 ? 6.0 : 4.0) * n);
+  // bytes: with lr +0.0 or positive and finite only the named elements are
+  // touched, 14 (or 12) bytes per word, which the host cannot count without
+  // reading the count: none are recorded here; otherwise the master read and
+  // written and the bf16 copy written (the words not counted)
+  const uint32_t lb = __builtin_bit_cast(uint32_t, lr);
+  const bool named_only = lb == 0u || (lr > 0.f && lr <= 3.402823466e38f);
+  Timed tm(AM_K_SGD, s, named_only ? 0.0 : 2.0 * n, named_only ? 0.0 : (weights_bf16 ? 10.0 : 8.0) * n);
   return hip_check(am::gtc_decode_sgd(words, count, capacity, tau, n, lr, master,
                                       static_cast<uint16_t*>(weights_bf16), s),
                    "decode + sgd");

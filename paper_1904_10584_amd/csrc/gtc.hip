@@ -270,17 +270,17 @@ __global__ __launch_bounds__(TPB) void gtc_decode_tiles(const uint32_t* __restri
 }
 
 
-// Decode of one stream fused with the SGD step: each tile's update is built
-// in LDS as in gtc_decode_tiles (accumulate = 0) and applied to the master
-// weights at once, so the dense update never goes to memory.  An element no
-// word names has update +0.0, and fl32(w - lr * 0.0) = w for every non-NaN w
-// when lr is +0.0 or positive and finite (SKIP): its master is then not
-// stored again; the bf16 copy is written for every element, as sgd_apply
-// does.  Same results as the two launches, bit for bit.
+// Decode of one stream fused with the SGD step, for a learning rate that is
+// -0.0, negative, infinite or NaN (then w - lr * 0.0 may differ from w, so
+// every element is rewritten): each tile's update is built in LDS as in
+// gtc_decode_tiles (accumulate = 0) and applied to every master weight of
+// the tile at once, so the dense update never goes to memory; the bf16 copy
+// is written for every element, as sgd_apply does.  Same results as the two
+// launches, bit for bit.
 template <bool ALIGNED, bool BF16>
 __global__ __launch_bounds__(TPB) void gtc_decode_sgd_tiles(
     const uint32_t* __restrict__ words, const int64_t* __restrict__ count, int64_t capacity,
-    float tau, int64_t n, float lr, bool skip, float* __restrict__ master, bf16_t* __restrict__ wb) {
+    float tau, int64_t n, float lr, float* __restrict__ master, bf16_t* __restrict__ wb) {
   __shared__ float tile[TILE];
   __shared__ int64_t range[2];
   const int64_t base = (int64_t)blockIdx.x * TILE;
@@ -304,8 +304,6 @@ __global__ __launch_bounds__(TPB) void gtc_decode_sgd_tiles(
   }
   __syncthreads();
   const double lr64 = (double)lr;
-  // stored again: any update bit set (including -0.0), a NaN, or no SKIP
-  auto keep = [&](float m, float u) { return skip && __float_as_uint(u) == 0u && m == m; };
   for (int i = threadIdx.x * 4; i < len; i += TPB * 4) {
     float* mp = master + base + i;
     if (ALIGNED && i + 3 < len) {
@@ -313,8 +311,7 @@ __global__ __launch_bounds__(TPB) void gtc_decode_sgd_tiles(
       const float4 u = *reinterpret_cast<const float4*>(tile + i);
       const float4 w = make_float4(sgd_one(m.x, u.x, lr64), sgd_one(m.y, u.y, lr64),
                                    sgd_one(m.z, u.z, lr64), sgd_one(m.w, u.w, lr64));
-      if (!(keep(m.x, u.x) && keep(m.y, u.y) && keep(m.z, u.z) && keep(m.w, u.w)))
-        *reinterpret_cast<float4*>(mp) = w;
+      *reinterpret_cast<float4*>(mp) = w;
       if (BF16) {
         uint2 b;
         b.x = (uint32_t)f32_to_bf16(w.x) | ((uint32_t)f32_to_bf16(w.y) << 16);
@@ -325,7 +322,7 @@ __global__ __launch_bounds__(TPB) void gtc_decode_sgd_tiles(
       for (int k = 0; k < 4 && i + k < len; ++k) {
         const float m = mp[k], u = tile[i + k];
         const float w = sgd_one(m, u, lr64);
-        if (!keep(m, u)) mp[k] = w;
+        mp[k] = w;
         if (BF16) wb[base + i + k] = f32_to_bf16(w);
       }
     }
@@ -461,6 +458,42 @@ hipError_t gtc_decode_multi(int streams, const uint32_t* words, int64_t capacity
   return hipGetLastError();
 }
 
+// The same step when lr is +0.0 or positive and finite: an element no word
+// names keeps its master (fl32(w - lr * 0.0) = w for non-NaN w), and its bf16
+// copy already holds that master's rounding, so only the named elements are
+// read and written.  Block t takes the words of tile t (found as in the
+// decoder) and, for each, loads the master, applies the step and stores the
+// master and its bf16 copy: about 14 bytes per sent element instead of a
+// pass over all n.
+template <bool BF16>
+__global__ __launch_bounds__(TPB) void gtc_decode_sgd_named(
+    const uint32_t* __restrict__ words, const int64_t* __restrict__ count, int64_t capacity,
+    float tau, int64_t n, float lr, float* __restrict__ master, bf16_t* __restrict__ wb) {
+  __shared__ int64_t range[2];
+  const int64_t base = (int64_t)blockIdx.x * TILE;
+  const int64_t len = n - base < TILE ? n - base : TILE;
+  if (threadIdx.x < 128) {  // wave 0: the tile's first word, wave 1: the next tile's
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    int64_t cnt = *count;
+    cnt = cnt < 0 ? 0 : (cnt > capacity ? capacity : cnt);
+    const int64_t end = base + (wv ? len : 0);
+    const int64_t r = lower_bound_wave(words, cnt, (uint32_t)(end << 1), lane);
+    if (lane == 0) range[wv] = r;
+  }
+  __syncthreads();
+  const int64_t lo = range[0], hi = range[1];
+  const double lr64 = (double)lr;
+  for (int64_t w = lo + threadIdx.x; w < hi; w += TPB) {
+    const uint32_t word = words[w];
+    const int i = (int)((word >> 1) - (uint32_t)base);
+    if ((unsigned)i >= (unsigned)len) continue;  // only for unsorted input
+    const int64_t e = base + i;
+    const float v = sgd_one(master[e], (word & 1u) ? -tau : tau, lr64);
+    master[e] = v;
+    if (BF16) wb[e] = f32_to_bf16(v);
+  }
+}
+
 hipError_t gtc_decode_sgd(const uint32_t* words, const int64_t* count, int64_t capacity, float tau,
                           int64_t n, float lr, float* master, uint16_t* w_bf16, hipStream_t s) {
   const int64_t ntiles = gtc_tiles(n);
@@ -468,17 +501,25 @@ hipError_t gtc_decode_sgd(const uint32_t* words, const int64_t* count, int64_t c
   const bool al = (reinterpret_cast<uintptr_t>(master) & 15) == 0 &&
                   (reinterpret_cast<uintptr_t>(w_bf16) & 7) == 0;
   const uint32_t lb = __builtin_bit_cast(uint32_t, lr);
-  const bool skip = lb == 0u || (lr > 0.f && lr <= 3.402823466e38f);
+  // +0.0 or positive and finite: only the named elements change
+  const bool named_only = lb == 0u || (lr > 0.f && lr <= 3.402823466e38f);
   bf16_t* wb = reinterpret_cast<bf16_t*>(w_bf16);
   const dim3 g((unsigned)ntiles), b(TPB);
+  if (named_only) {
+    if (wb)
+      hipLaunchKernelGGL(gtc_decode_sgd_named<true>, g, b, 0, s, words, count, capacity, tau, n, lr, master, wb);
+    else
+      hipLaunchKernelGGL(gtc_decode_sgd_named<false>, g, b, 0, s, words, count, capacity, tau, n, lr, master, wb);
+    return hipGetLastError();
+  }
   if (al && wb)
-    hipLaunchKernelGGL((gtc_decode_sgd_tiles<true, true>), g, b, 0, s, words, count, capacity, tau, n, lr, skip, master, wb);
+    hipLaunchKernelGGL((gtc_decode_sgd_tiles<true, true>), g, b, 0, s, words, count, capacity, tau, n, lr, master, wb);
   else if (al)
-    hipLaunchKernelGGL((gtc_decode_sgd_tiles<true, false>), g, b, 0, s, words, count, capacity, tau, n, lr, skip, master, wb);
+    hipLaunchKernelGGL((gtc_decode_sgd_tiles<true, false>), g, b, 0, s, words, count, capacity, tau, n, lr, master, wb);
   else if (wb)
-    hipLaunchKernelGGL((gtc_decode_sgd_tiles<false, true>), g, b, 0, s, words, count, capacity, tau, n, lr, skip, master, wb);
+    hipLaunchKernelGGL((gtc_decode_sgd_tiles<false, true>), g, b, 0, s, words, count, capacity, tau, n, lr, master, wb);
   else
-    hipLaunchKernelGGL((gtc_decode_sgd_tiles<false, false>), g, b, 0, s, words, count, capacity, tau, n, lr, skip, master, wb);
+    hipLaunchKernelGGL((gtc_decode_sgd_tiles<false, false>), g, b, 0, s, words, count, capacity, tau, n, lr, master, wb);
   return hipGetLastError();
 }
 

@@ -152,14 +152,25 @@ def test_decode_bit_exact(n, accumulate):
     np.testing.assert_array_equal(_bits32(dense.cpu().numpy()), _bits32(ref))
 
 
+def _bf16_rounding(m):
+    """The library's bf16 rounding of the masters m (sgd_apply with lr 0 and
+    a zero update), i.e. the copy an SGD call leaves; torch's own conversion
+    differs at NaN."""
+    scratch = to_dev(m.copy())
+    b = torch.empty(m.shape[0], dtype=torch.bfloat16, device="cuda")
+    am.sgd_apply(scratch, torch.zeros_like(scratch), 0.0, b)
+    return b
+
+
 @pytest.mark.parametrize("n,offset", [(1, 0), (4097, 1), (1_000_003, 0)])
 @pytest.mark.parametrize("lr", [0.01, 0.0, -0.0, -0.5, float("nan"), float("inf")])
 @pytest.mark.parametrize("with_bf16", [True, False])
 def test_decode_sgd_matches_decode_then_sgd(n, offset, lr, with_bf16):
     """The fused pass against the two calls on the GPU (bit for bit, master
     values with NaNs and signed zeros; the learning rates that are not +0.0
-    or positive and finite turn off its skipping of unnamed elements) and,
-    for finite values, against the oracle's decode followed by its SGD."""
+    or positive and finite make it rewrite every element) and, for finite
+    values, against the oracle's decode followed by its SGD.  The bf16 copies
+    start as the masters' rounding, the state every SGD call leaves them in."""
     say(f"decode+sgd n={n} offset={offset} lr={lr} bf16={with_bf16}")
     rng = np.random.default_rng(n + offset)
     tau = np.float32(1e-3)
@@ -172,8 +183,8 @@ def test_decode_sgd_matches_decode_then_sgd(n, offset, lr, with_bf16):
     lr32 = np.float32(lr)
     fused = to_dev(m0)
     two = to_dev(m0)
-    fb = torch.zeros(n + offset, dtype=torch.bfloat16, device="cuda") if with_bf16 else None
-    tb = torch.zeros(n + offset, dtype=torch.bfloat16, device="cuda") if with_bf16 else None
+    fb = _bf16_rounding(m0) if with_bf16 else None
+    tb = _bf16_rounding(m0) if with_bf16 else None
     am.grad_threshold_decode_sgd(words, count, tau, fused[offset:], lr32,
                                  fb[offset:] if with_bf16 else None)
     dense = torch.full((n,), 7.0, dtype=torch.float32, device="cuda")
@@ -191,6 +202,38 @@ def test_decode_sgd_matches_decode_then_sgd(n, offset, lr, with_bf16):
         if with_bf16:
             got_b = fb.cpu().view(torch.int16).numpy().view(np.uint16)[offset:]
             np.testing.assert_array_equal(got_b[finite], ref_b[finite])
+
+
+@pytest.mark.parametrize("lr", [0.01, -0.5])
+def test_decode_sgd_touches_only_named_elements(lr):
+    """With lr +0.0 or positive and finite only the elements a word names are
+    written (master and bf16 copy); every other element keeps both, here a
+    bf16 sentinel that is not the master's rounding.  With any other lr
+    every element is rewritten, as decode then SGD would."""
+    n = 300_001
+    rng = np.random.default_rng(11)
+    tau = np.float32(1e-3)
+    g = (rng.standard_normal(n) * 1.2e-3).astype(np.float32)
+    _, ref_w, ref_c = oracle.grad_threshold_encode(g, np.zeros(n, np.float32), tau)
+    _, _, c, words, count = _encode_gpu(g, np.zeros(n, np.float32), tau)
+    assert c == ref_c and 0 < c < n
+    m0 = rng.standard_normal(n).astype(np.float32)
+    master = to_dev(m0)
+    wb = torch.full((n,), 0x1234, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+    am.grad_threshold_decode_sgd(words, count, tau, master, np.float32(lr), wb)
+    u = oracle.grad_threshold_decode(ref_w, ref_c, tau, n)
+    ref_m, ref_b = oracle.sgd_apply(m0, u, np.float32(lr))
+    named = np.zeros(n, bool)
+    named[(ref_w[:ref_c] >> 1).astype(np.int64)] = True
+    got_m = master.cpu().numpy()
+    got_b = wb.cpu().view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(_bits32(got_m), _bits32(ref_m))
+    np.testing.assert_array_equal(got_b[named], ref_b[named])
+    if lr > 0:
+        assert np.all(got_b[~named] == 0x1234)
+        np.testing.assert_array_equal(_bits32(got_m[~named]), _bits32(m0[~named]))
+    else:
+        np.testing.assert_array_equal(got_b, ref_b)
 
 
 def test_decode_sgd_count_clamped_to_capacity():
