@@ -540,10 +540,10 @@ __global__ __launch_bounds__(512, 1) void lstm_bwd_xcd(PersistBwd a, PersistSche
     const int off_prev = off - nb_prev;
 
     // This wave's cell inputs (independent of the exchange), issued after
-    // the first two chunks' direct loads so that the chunk waits can leave
-    // them in flight: NL loads, the same number in every wave (clamped
-    // addresses for items past the wave's last), which the wait counts below
-    // assume.  Issued before the exchange instead, they would sit ahead of
+    // the first NB chunks' direct loads so that the chunk waits can leave
+    // them in flight: NL loads (one instruction each), the same number in
+    // every wave (clamped addresses for items past the wave's last), which
+    // the wait counts below assume.  Issued before the exchange instead, they would sit ahead of
     // the chunks in the in-order memory counter and hold up the product.
     bf16_t gv[IPS][4], dhv[IPS];
     float cv[IPS], cpv[IPS];
